@@ -1,0 +1,169 @@
+/*
+ * embbag.h — C ABI of the MI355X (gfx950) EmbeddingBag training step.
+ *
+ * Operators (Kalamkar et al., "Optimizing Deep Learning Recommender Systems'
+ * Training on CPU Cluster Architectures", arXiv 2005.04680):
+ *   - forward: sum-pooled gather over many tables (Section III-A,
+ *     Algorithm 1; Section II's L = A^T W over the bags of a minibatch);
+ *   - backward fused with the sparse SGD update of only the touched rows
+ *     (Algorithms 2 and 3, whose fusion the end of Section III-A describes;
+ *     every row receives the sum of all its look-ups' gradients exactly once,
+ *     the single-writer property of Algorithm 4, here without float atomics);
+ *   - the Split-SGD-BF16 variants of both (Section VII).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Tables.  T tables (1 <= T <= 64) of M_t rows (1 <= M_t, sum of M_t <=
+ *   2^31 - 1) and dimension E (4 <= E <= 1024, E % 4 == 0).  An FP32 table is a
+ *   row-major [M_t][E] device array, 16-byte aligned.  A split table is two
+ *   row-major [M_t][E] uint16 device arrays, 8-byte aligned: `hi` holds the 16
+ *   most significant bits of each FP32 weight (a BF16 number, by truncation)
+ *   and `lo` the 16 least significant bits (Section VII stores them as two
+ *   separate tensors).
+ * Bags.  `batch` = B bags per table.  Bag k = t*B + b reads
+ *   indices[offsets[k] .. offsets[k+1]) (half-open), rows of table t.
+ *   `indices`: device int32 [num_indices], table-local rows.
+ *   `offsets`: device int32 [T*B + 1], offsets[0] == 0, non-decreasing,
+ *   offsets[T*B] == num_indices.  (Algorithm 1's header swaps the two sizes;
+ *   its loops read O[n] and O[n+1].)  A row may repeat within and across
+ *   bags; repeats count with multiplicity.  An empty bag pools to +0.0.
+ * Pooled data.  `pooled_out` and `grad_pooled`: device FP32 [T][B][E],
+ *   contiguous, 16-byte aligned.
+ * Streams.  Every call only enqueues work on `stream` (0 = the null stream)
+ *   and returns; the caller keeps all buffers alive until that work is done.
+ *   The only call that waits is embbag_status_read.
+ * Ownership.  The caller owns every buffer.  The library allocates no device
+ *   memory, keeps no pointer after returning and holds no global state, so
+ *   calls on distinct workspaces are thread-safe.  Tables are updated in
+ *   place; `pooled_out` must not alias a table.
+ * Errors.  Argument errors (null pointers, sizes out of range, a workspace
+ *   that is too small or misaligned) are found on the host: the call returns
+ *   the code and enqueues nothing.  Data errors (bad offsets, an index out of
+ *   its table's range) are found on the device: the call returns EMBBAG_OK,
+ *   and the device lowers `*d_status` to min(*d_status, code) (the caller
+ *   zeroes it; EMBBAG_ERR_OFFSETS wins over EMBBAG_ERR_INDEX_RANGE).  After a
+ *   data error the forward's output is unspecified and the backward writes no
+ *   table row at all.  Launch failures return EMBBAG_ERR_HIP.
+ */
+#ifndef EMBBAG_H_
+#define EMBBAG_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define EMBBAG_OK 0
+#define EMBBAG_ERR_INVALID_ARG (-1) /* null pointer, T/E/B/sizes out of range */
+#define EMBBAG_ERR_WORKSPACE (-2)   /* workspace smaller than required, or not 256-B aligned */
+#define EMBBAG_ERR_INDEX_RANGE (-3) /* an index outside [0, M_t) (device-detected) */
+#define EMBBAG_ERR_OFFSETS (-4)     /* offsets[0] != 0, decreasing, or offsets[T*B] != num_indices */
+#define EMBBAG_ERR_HIP (-5)         /* a HIP launch or runtime call failed */
+
+/* Static string naming a status code ("unknown status" otherwise). */
+const char* embbag_status_string(int code);
+
+/* FP32 tables.  `rows` and `weights` are HOST arrays of num_tables entries;
+ * weights[t] is a device pointer to rows[t] x dim floats. */
+typedef struct {
+  int32_t num_tables;
+  int32_t dim;
+  const int64_t* rows;
+  float* const* weights;
+} embbag_tables_t;
+
+/* Split-SGD-BF16 tables (Section VII): hi[t], lo[t] are device pointers to
+ * rows[t] x dim uint16 each. */
+typedef struct {
+  int32_t num_tables;
+  int32_t dim;
+  const int64_t* rows;
+  uint16_t* const* hi;
+  uint16_t* const* lo;
+} embbag_split_tables_t;
+
+/* Forward, Algorithm 1 (sum pooling): for every bag k = t*B + b,
+ *   pooled_out[t][b][:] = sum over s in [offsets[k], offsets[k+1]) of
+ *                         weights[t][indices[s]][:]        (+0.0 if empty).
+ * FP32 accumulation in look-up order within each lane's partial sums.
+ * `d_status` (device int32, nullable) receives data errors as described in
+ * the header comment. */
+int embbag_forward(const embbag_tables_t* tables, int32_t batch, const int32_t* indices,
+                   const int32_t* offsets, int64_t num_indices, float* pooled_out,
+                   int32_t* d_status, hipStream_t stream);
+
+/* Bytes of device workspace the backward (FP32 or split) needs for these
+ * sizes; 0 for invalid sizes.  The workspace must be 256-byte aligned. */
+size_t embbag_backward_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices,
+                                       int32_t dim);
+
+/* Fused backward + sparse SGD, Algorithms 2-3 with alpha = -lr:
+ * for every (table t, row r) named by at least one look-up,
+ *   weights[t][r][:] -= lr * sum over look-ups s with indices[s] == r in a
+ *                       bag k of table t of grad_pooled[k][:],
+ * each touched row read and written exactly once (no float atomics; the
+ * gradient sum is accumulated in FP64 and rounded once).  Rows no look-up
+ * names are not written.  `workspace` (device, >= embbag_backward_workspace_bytes)
+ * is scratch owned by the caller.  `d_status` is nullable. */
+int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* indices,
+                        const int32_t* offsets, int64_t num_indices, float lr,
+                        const embbag_tables_t* tables, void* workspace, size_t workspace_bytes,
+                        int32_t* d_status, hipStream_t stream);
+
+/* Forward of Section VII: Algorithm 1 reading only the BF16 high halves
+ * (each value is hi << 16 as FP32); the low halves are not read. */
+int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch,
+                              const int32_t* indices, const int32_t* offsets,
+                              int64_t num_indices, float* pooled_out, int32_t* d_status,
+                              hipStream_t stream);
+
+/* Update of Section VII: for every touched row, recombine hi/lo into the FP32
+ * weight, apply the same update as embbag_backward_sgd in FP32, and split the
+ * result back into hi/lo.  Untouched rows keep both halves. */
+int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
+                                   const int32_t* indices, const int32_t* offsets,
+                                   int64_t num_indices, float lr,
+                                   const embbag_split_tables_t* tables, void* workspace,
+                                   size_t workspace_bytes, int32_t* d_status,
+                                   hipStream_t stream);
+
+/* Section VII storage helpers (device, elementwise over n values):
+ * hi[i] = bits(w[i]) >> 16, lo[i] = bits(w[i]) & 0xFFFF, and the inverse
+ * w[i] = from_bits(hi[i] << 16 | lo[i]).  Lossless in both directions. */
+int embbag_split_fp32(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t stream);
+int embbag_combine_fp32(const uint16_t* hi, const uint16_t* lo, float* w, int64_t n,
+                        hipStream_t stream);
+
+/* Bytes of device workspace embbag_dedup needs (256-byte aligned). */
+size_t embbag_dedup_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices);
+
+/* Integer work of the backward, exposed for bit-exact checking:
+ *   key[s] = rowbase[t] + indices[s] (rowbase = exclusive prefix sum of rows),
+ *   bag[s] = k for offsets[k] <= s < offsets[k+1];
+ *   (sorted_keys, sorted_bags)[NS] = (key, bag) stably sorted by key (ties in
+ *     increasing s);
+ *   unique_keys[U] = the distinct keys, increasing; seg_off[U+1] = first sorted
+ *     position of each, seg_off[U] = NS; *d_num_unique = U.
+ * All outputs are device arrays sized for the worst case (U = NS):
+ * sorted_keys, sorted_bags, unique_keys [NS] uint32, seg_off [NS+1] int32,
+ * d_num_unique one int32.  `rows` is a HOST array of num_tables entries. */
+int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const int32_t* indices,
+                 const int32_t* offsets, int64_t num_indices, uint32_t* sorted_keys,
+                 uint32_t* sorted_bags, uint32_t* unique_keys, int32_t* seg_off,
+                 int32_t* d_num_unique, void* workspace, size_t workspace_bytes,
+                 int32_t* d_status, hipStream_t stream);
+
+/* Waits for `stream` and returns the device status word (*d_status), or
+ * EMBBAG_ERR_HIP if the wait or copy fails. */
+int embbag_status_read(const int32_t* d_status, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMBBAG_H_ */

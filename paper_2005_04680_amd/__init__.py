@@ -1,0 +1,234 @@
+"""MI355X (gfx950) EmbeddingBag training step — thin Python binding.
+
+Argument marshalling only: every function takes torch tensors that live on
+the GPU, passes their device pointers and the current HIP stream to the C ABI
+of ``libembbag.so`` (declared in ``include/embbag.h``) and returns its status
+code.  All computation happens in the library's HIP kernels; there is no CPU
+path, and loading fails loudly when the library has not been built.
+
+Operators (arXiv 2005.04680): Algorithm 1 (sum-pooled forward), Algorithms
+2-3 fused into one backward + sparse SGD update of the touched rows, and the
+Split-SGD-BF16 storage of Section VII.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libembbag.so")
+
+EMBBAG_OK = 0
+EMBBAG_ERR_INVALID_ARG = -1
+EMBBAG_ERR_WORKSPACE = -2
+EMBBAG_ERR_INDEX_RANGE = -3
+EMBBAG_ERR_OFFSETS = -4
+EMBBAG_ERR_HIP = -5
+
+
+class EmbbagError(RuntimeError):
+    def __init__(self, code: int, where: str = ""):
+        super().__init__(f"{where}: {embbag_status_string(code)} ({code})")
+        self.code = code
+
+
+class _Tables(C.Structure):
+    _fields_ = [("num_tables", C.c_int32), ("dim", C.c_int32),
+                ("rows", C.POINTER(C.c_int64)), ("weights", C.POINTER(C.c_void_p))]
+
+
+class _SplitTables(C.Structure):
+    _fields_ = [("num_tables", C.c_int32), ("dim", C.c_int32),
+                ("rows", C.POINTER(C.c_int64)), ("hi", C.POINTER(C.c_void_p)),
+                ("lo", C.POINTER(C.c_void_p))]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libembbag.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2005_04680_amd.build` (hipcc, gfx950)")
+        L = C.CDLL(LIB_PATH)
+        p, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+        L.embbag_status_string.argtypes = [C.c_int]
+        L.embbag_status_string.restype = C.c_char_p
+        L.embbag_forward.argtypes = [p, i32, p, p, i64, p, p, p]
+        L.embbag_forward_split_bf16.argtypes = [p, i32, p, p, i64, p, p, p]
+        L.embbag_backward_workspace_bytes.argtypes = [i32, i32, i64, i32]
+        L.embbag_backward_workspace_bytes.restype = sz
+        L.embbag_backward_sgd.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz, p, p]
+        L.embbag_backward_sgd_split_bf16.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz, p, p]
+        L.embbag_split_fp32.argtypes = [p, p, p, i64, p]
+        L.embbag_combine_fp32.argtypes = [p, p, p, i64, p]
+        L.embbag_dedup_workspace_bytes.argtypes = [i32, i32, i64]
+        L.embbag_dedup_workspace_bytes.restype = sz
+        L.embbag_dedup.argtypes = [i32, p, i32, p, p, i64, p, p, p, p, p, p, sz, p, p]
+        L.embbag_status_read.argtypes = [p, p]
+        for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
+                  "embbag_backward_sgd_split_bf16", "embbag_split_fp32", "embbag_combine_fp32",
+                  "embbag_dedup", "embbag_status_read"):
+            getattr(L, n).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def embbag_status_string(code: int) -> str:
+    return lib().embbag_status_string(int(code)).decode()
+
+
+def check(code: int, where: str = "embbag") -> None:
+    if code != EMBBAG_OK:
+        raise EmbbagError(code, where)
+
+
+# ---- marshalling helpers ---------------------------------------------------
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _ptr(t, dtypes=None, name="tensor"):
+    """Device pointer of a contiguous GPU tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    return t.data_ptr()
+
+
+def _dt(*names):
+    import torch
+    return tuple(getattr(torch, n) for n in names if hasattr(torch, n))
+
+
+def _tables_struct(tables, split_lo=None):
+    import torch
+    T = len(tables)
+    rows = (C.c_int64 * max(T, 1))(*[int(t.shape[0]) for t in tables])
+    dim = int(tables[0].shape[1]) if T else 0
+    ptrs = (C.c_void_p * max(T, 1))(*[_ptr(t, None, "table") for t in tables])
+    keep = [rows, ptrs]
+    if split_lo is None:
+        for t in tables:
+            if t.dtype != torch.float32:
+                raise TypeError("FP32 tables expected")
+        s = _Tables(T, dim, C.cast(rows, C.POINTER(C.c_int64)), C.cast(ptrs, C.POINTER(C.c_void_p)))
+    else:
+        lo = (C.c_void_p * max(T, 1))(*[_ptr(t, None, "lo table") for t in split_lo])
+        keep.append(lo)
+        s = _SplitTables(T, dim, C.cast(rows, C.POINTER(C.c_int64)),
+                         C.cast(ptrs, C.POINTER(C.c_void_p)), C.cast(lo, C.POINTER(C.c_void_p)))
+    return s, keep
+
+
+def _split_struct_fwd(hi):
+    T = len(hi)
+    rows = (C.c_int64 * max(T, 1))(*[int(t.shape[0]) for t in hi])
+    ptrs = (C.c_void_p * max(T, 1))(*[_ptr(t, None, "hi table") for t in hi])
+    s = _SplitTables(T, int(hi[0].shape[1]) if T else 0, C.cast(rows, C.POINTER(C.c_int64)),
+                     C.cast(ptrs, C.POINTER(C.c_void_p)), None)
+    return s, [rows, ptrs]
+
+
+_I32 = ("int32",)
+_U16 = ("uint16", "int16")
+_U32 = ("uint32", "int32")
+
+
+# ---- entry points (same names as the C ABI) --------------------------------
+def embbag_forward(weights, batch, indices, offsets, pooled_out, d_status=None, stream=None) -> int:
+    """Algorithm 1 over FP32 tables ``weights`` (list of [M_t, E] tensors)."""
+    s, keep = _tables_struct(weights)
+    return lib().embbag_forward(C.byref(s), int(batch), _ptr(indices, _dt(*_I32), "indices"),
+                                _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
+                                _ptr(pooled_out, _dt("float32"), "pooled_out"),
+                                _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_forward_split_bf16(hi, batch, indices, offsets, pooled_out, d_status=None,
+                              stream=None) -> int:
+    s, keep = _split_struct_fwd(hi)
+    return lib().embbag_forward_split_bf16(C.byref(s), int(batch),
+                                           _ptr(indices, _dt(*_I32), "indices"),
+                                           _ptr(offsets, _dt(*_I32), "offsets"),
+                                           int(indices.numel()),
+                                           _ptr(pooled_out, _dt("float32"), "pooled_out"),
+                                           _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_workspace_bytes(num_tables, batch, num_indices, dim) -> int:
+    return int(lib().embbag_backward_workspace_bytes(int(num_tables), int(batch),
+                                                     int(num_indices), int(dim)))
+
+
+def embbag_backward_sgd(grad_pooled, batch, indices, offsets, lr, weights, workspace,
+                        d_status=None, stream=None) -> int:
+    """Fused backward + SGD; ``weights`` are updated in place."""
+    s, keep = _tables_struct(weights)
+    return lib().embbag_backward_sgd(_ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
+                                     _ptr(indices, _dt(*_I32), "indices"),
+                                     _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
+                                     float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
+                                     int(workspace.numel() * workspace.element_size()),
+                                     _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_sgd_split_bf16(grad_pooled, batch, indices, offsets, lr, hi, lo, workspace,
+                                   d_status=None, stream=None) -> int:
+    s, keep = _tables_struct(hi, split_lo=lo)
+    return lib().embbag_backward_sgd_split_bf16(
+        _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
+        _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
+        int(indices.numel()), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
+        int(workspace.numel() * workspace.element_size()),
+        _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_split_fp32(w, hi, lo, stream=None) -> int:
+    return lib().embbag_split_fp32(_ptr(w, _dt("float32"), "w"), _ptr(hi, _dt(*_U16), "hi"),
+                                   _ptr(lo, _dt(*_U16), "lo"), int(w.numel()), _stream(stream))
+
+
+def embbag_combine_fp32(hi, lo, w, stream=None) -> int:
+    return lib().embbag_combine_fp32(_ptr(hi, _dt(*_U16), "hi"), _ptr(lo, _dt(*_U16), "lo"),
+                                     _ptr(w, _dt("float32"), "w"), int(w.numel()), _stream(stream))
+
+
+def embbag_dedup_workspace_bytes(num_tables, batch, num_indices) -> int:
+    return int(lib().embbag_dedup_workspace_bytes(int(num_tables), int(batch), int(num_indices)))
+
+
+def embbag_dedup(rows, batch, indices, offsets, sorted_keys, sorted_bags, unique_keys, seg_off,
+                 d_num_unique, workspace, d_status=None, stream=None) -> int:
+    T = len(rows)
+    r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
+    return lib().embbag_dedup(T, C.cast(r, C.c_void_p), int(batch),
+                              _ptr(indices, _dt(*_I32), "indices"),
+                              _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
+                              _ptr(sorted_keys, _dt(*_U32), "sorted_keys"),
+                              _ptr(sorted_bags, _dt(*_U32), "sorted_bags"),
+                              _ptr(unique_keys, _dt(*_U32), "unique_keys"),
+                              _ptr(seg_off, _dt(*_I32), "seg_off"),
+                              _ptr(d_num_unique, _dt(*_I32), "d_num_unique"),
+                              _ptr(workspace, None, "workspace"),
+                              int(workspace.numel() * workspace.element_size()),
+                              _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_status_read(d_status, stream=None) -> int:
+    return lib().embbag_status_read(_ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+__all__ = [n for n in dir() if n.startswith("embbag_") or n.startswith("EMBBAG_")] + [
+    "lib", "check", "EmbbagError", "LIB_PATH"]

@@ -1,0 +1,253 @@
+// C ABI of the EmbeddingBag library: argument checks, workspace layout and
+// the launch sequence of each entry point on the caller's stream.
+#include <cstring>
+
+#include "common.hpp"
+
+using namespace embbag;
+
+namespace {
+
+constexpr int64_t kInt32Max = 2147483647;
+constexpr size_t kWsAlign = 256;
+
+bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Table shapes (and, when `w` is given, the per-table device pointers).
+int make_desc(int32_t T, int32_t E, const int64_t* rows, void* const* w, void* const* lo,
+              size_t align, TableDesc* d) {
+  if (T < 1 || T > kMaxTables) return EMBBAG_ERR_INVALID_ARG;
+  if (E < 4 || E > 1024 || E % 4 != 0) return EMBBAG_ERR_INVALID_ARG;
+  if (rows == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  std::memset(d, 0, sizeof(*d));
+  int64_t total = 0;
+  for (int t = 0; t < T; ++t) {
+    if (rows[t] < 1 || rows[t] > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+    if (align != 0) {
+      if (w == nullptr || w[t] == nullptr || !aligned(w[t], align)) return EMBBAG_ERR_INVALID_ARG;
+      d->w[t] = w[t];
+      if (lo != nullptr) {
+        if (lo[t] == nullptr || !aligned(lo[t], align)) return EMBBAG_ERR_INVALID_ARG;
+        d->lo[t] = lo[t];
+      }
+    }
+    d->rows[t] = uint32_t(rows[t]);
+    d->rowbase[t] = uint32_t(total);
+    total += rows[t];
+  }
+  if (total > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+  d->rowbase[T] = uint32_t(total);
+  d->num_tables = T;
+  d->dim = E;
+  return EMBBAG_OK;
+}
+
+int check_bags(int32_t T, int32_t B, const int32_t* I, const int32_t* O, int64_t NS) {
+  if (B < 0 || NS < 0 || NS > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+  if (int64_t(T) * B + 1 > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+  if (O == nullptr || (NS > 0 && I == nullptr)) return EMBBAG_ERR_INVALID_ARG;
+  // offsets[0] must be both 0 and num_indices: the sizes alone contradict.
+  if (int64_t(T) * B == 0 && NS > 0) return EMBBAG_ERR_OFFSETS;
+  return EMBBAG_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? EMBBAG_OK : EMBBAG_ERR_HIP; }
+
+int forward_common(const TableDesc& d, bool split, int32_t B, const int32_t* I, const int32_t* O,
+                   int64_t NS, float* Y, int32_t* d_status, hipStream_t st) {
+  int rc = check_bags(d.num_tables, B, I, O, NS);
+  if (rc) return rc;
+  if (int64_t(d.num_tables) * B > 0 && (Y == nullptr || !aligned(Y, 16)))
+    return EMBBAG_ERR_INVALID_ARG;
+  return hip_status(launch_forward(d, split, B, I, O, NS, Y, d_status, st));
+}
+
+int backward_common(const TableDesc& d, bool split, const float* dY, int32_t B, const int32_t* I,
+                    const int32_t* O, int64_t NS, float lr, void* ws, size_t ws_bytes,
+                    int32_t* d_status, hipStream_t st) {
+  int rc = check_bags(d.num_tables, B, I, O, NS);
+  if (rc) return rc;
+  if (NS > 0 && (dY == nullptr || !aligned(dY, 16))) return EMBBAG_ERR_INVALID_ARG;
+  const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, d.rowbase[d.num_tables], false);
+  if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
+  char* w = static_cast<char*>(ws);
+  uint64_t* sorted = nullptr;
+  hipError_t e = launch_sort(d, B, I, O, NS, L, w, d_status, st, &sorted);
+  if (e != hipSuccess) return EMBBAG_ERR_HIP;
+  return hip_status(launch_segment_sgd(d, split, B, dY, lr, sorted, L, w, st));
+}
+
+}  // namespace
+
+namespace embbag {
+
+BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
+                          bool for_dedup) {
+  (void)T;
+  (void)B;
+  BwdLayout L{};
+  L.ns = NS;
+  L.ntiles = (NS + kTile - 1) / kTile;
+  L.nkeyblocks = L.ntiles > 0 ? L.ntiles : 1;
+  // Chunk of the segmented reduce: ~16K chunks, 64..1024 look-ups each.
+  int64_t c = 64;
+  while (c < 1024 && c * 2 * 16384 <= NS) c *= 2;
+  L.chunk = c;
+  L.nchunks = (NS + c - 1) / c;
+  int nbits = 0;
+  if (total_rows > 1) nbits = 32 - __builtin_clz(total_rows - 1u);
+  L.passes = (nbits + kRadixBits - 1) / kRadixBits;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = round_up(off + bytes, kWsAlign);
+    return o;
+  };
+  L.off_a = take(size_t(NS) * 8);
+  L.off_b = take(size_t(NS) * 8);
+  L.off_hist = take(size_t(kRadix) * size_t(L.ntiles) * 4);
+  L.off_tot = take(size_t(kRadix) * 4);
+  L.off_parts = take(size_t(L.nkeyblocks) * 4);
+  L.off_flags = take(64);
+  L.off_carry = take(for_dedup ? 0 : size_t(2) * size_t(L.nchunks) * size_t(E) * 8);
+  L.off_uniq = take(for_dedup ? size_t(L.ntiles) * 4 : 0);
+  L.total = off;
+  return L;
+}
+
+}  // namespace embbag
+
+extern "C" {
+
+const char* embbag_status_string(int code) {
+  switch (code) {
+    case EMBBAG_OK: return "ok";
+    case EMBBAG_ERR_INVALID_ARG: return "invalid argument";
+    case EMBBAG_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case EMBBAG_ERR_INDEX_RANGE: return "index out of its table's range";
+    case EMBBAG_ERR_OFFSETS: return "invalid offsets";
+    case EMBBAG_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+int embbag_forward(const embbag_tables_t* tables, int32_t batch, const int32_t* indices,
+                   const int32_t* offsets, int64_t num_indices, float* pooled_out,
+                   int32_t* d_status, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, d_status,
+                        stream);
+}
+
+int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch,
+                              const int32_t* indices, const int32_t* offsets,
+                              int64_t num_indices, float* pooled_out, int32_t* d_status,
+                              hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->hi), nullptr, 8, &d);
+  if (rc) return rc;
+  return forward_common(d, true, batch, indices, offsets, num_indices, pooled_out, d_status,
+                        stream);
+}
+
+size_t embbag_backward_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices,
+                                       int32_t dim) {
+  if (num_tables < 1 || num_tables > kMaxTables || dim < 4 || dim > 1024 || dim % 4 != 0)
+    return 0;
+  if (batch < 0 || num_indices < 0 || num_indices > kInt32Max) return 0;
+  if (int64_t(num_tables) * batch + 1 > kInt32Max) return 0;
+  return backward_layout(num_tables, batch, num_indices, dim, 0, false).total;
+}
+
+int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* indices,
+                        const int32_t* offsets, int64_t num_indices, float lr,
+                        const embbag_tables_t* tables, void* workspace, size_t workspace_bytes,
+                        int32_t* d_status, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  return backward_common(d, false, grad_pooled, batch, indices, offsets, num_indices, lr,
+                         workspace, workspace_bytes, d_status, stream);
+}
+
+int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
+                                   const int32_t* indices, const int32_t* offsets,
+                                   int64_t num_indices, float lr,
+                                   const embbag_split_tables_t* tables, void* workspace,
+                                   size_t workspace_bytes, int32_t* d_status,
+                                   hipStream_t stream) {
+  if (tables == nullptr || tables->lo == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->hi),
+                     reinterpret_cast<void* const*>(tables->lo), 8, &d);
+  if (rc) return rc;
+  return backward_common(d, true, grad_pooled, batch, indices, offsets, num_indices, lr,
+                         workspace, workspace_bytes, d_status, stream);
+}
+
+int embbag_split_fp32(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t stream) {
+  if (n < 0 || (n > 0 && (w == nullptr || hi == nullptr || lo == nullptr)))
+    return EMBBAG_ERR_INVALID_ARG;
+  return hip_status(launch_split(w, hi, lo, n, stream));
+}
+
+int embbag_combine_fp32(const uint16_t* hi, const uint16_t* lo, float* w, int64_t n,
+                        hipStream_t stream) {
+  if (n < 0 || (n > 0 && (w == nullptr || hi == nullptr || lo == nullptr)))
+    return EMBBAG_ERR_INVALID_ARG;
+  return hip_status(launch_combine(hi, lo, w, n, stream));
+}
+
+size_t embbag_dedup_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices) {
+  if (num_tables < 1 || num_tables > kMaxTables) return 0;
+  if (batch < 0 || num_indices < 0 || num_indices > kInt32Max) return 0;
+  if (int64_t(num_tables) * batch + 1 > kInt32Max) return 0;
+  return backward_layout(num_tables, batch, num_indices, 4, 0, true).total;
+}
+
+int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const int32_t* indices,
+                 const int32_t* offsets, int64_t num_indices, uint32_t* sorted_keys,
+                 uint32_t* sorted_bags, uint32_t* unique_keys, int32_t* seg_off,
+                 int32_t* d_num_unique, void* workspace, size_t workspace_bytes,
+                 int32_t* d_status, hipStream_t stream) {
+  TableDesc d;
+  int rc = make_desc(num_tables, 4, rows, nullptr, nullptr, 0, &d);
+  if (rc) return rc;
+  rc = check_bags(num_tables, batch, indices, offsets, num_indices);
+  if (rc) return rc;
+  if (seg_off == nullptr || d_num_unique == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  if (num_indices > 0 && (sorted_keys == nullptr || sorted_bags == nullptr || unique_keys == nullptr))
+    return EMBBAG_ERR_INVALID_ARG;
+  const BwdLayout L = backward_layout(num_tables, batch, num_indices, 4, d.rowbase[num_tables], true);
+  if (workspace == nullptr || !aligned(workspace, kWsAlign) || workspace_bytes < L.total)
+    return EMBBAG_ERR_WORKSPACE;
+  char* w = static_cast<char*>(workspace);
+  uint64_t* sorted = nullptr;
+  if (launch_sort(d, batch, indices, offsets, num_indices, L, w, d_status, stream, &sorted) !=
+      hipSuccess)
+    return EMBBAG_ERR_HIP;
+  return hip_status(launch_unique(sorted, L, w, sorted_keys, sorted_bags, unique_keys, seg_off,
+                                  d_num_unique, stream));
+}
+
+int embbag_status_read(const int32_t* d_status, hipStream_t stream) {
+  if (d_status == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  if (hipStreamSynchronize(stream) != hipSuccess) return EMBBAG_ERR_HIP;
+  int32_t v = 0;
+  if (hipMemcpy(&v, d_status, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess)
+    return EMBBAG_ERR_HIP;
+  return v;
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Internal definitions shared by the gfx950 kernels and the host launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "embbag.h"
+
+namespace embbag {
+
+constexpr int kMaxTables = 64;
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kBlock = 256;        // threads per workgroup (4 waves)
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kNumXcd = 8;         // MI355X: 8 XCDs, each with its own L2
+
+// Radix sort geometry: 8-bit digits, 4096-key tiles (256 threads x 16 keys).
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+constexpr int kItemsPerThread = 16;
+constexpr int kTile = kBlock * kItemsPerThread;
+
+// Sentinel for "no key": keys are < 2^31 because sum(M_t) < 2^31.
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef double d4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+// Table descriptor, passed by value as a kernel argument (kernarg segment).
+// For FP32 tables `w[t]` is the table; for split tables `w[t]` is the BF16
+// high half and `lo[t]` the low half.
+struct TableDesc {
+  void* w[kMaxTables];
+  void* lo[kMaxTables];
+  uint32_t rows[kMaxTables];
+  uint32_t rowbase[kMaxTables + 1];
+  int32_t num_tables;
+  int32_t dim;
+};
+
+// Lane geometry for a row of E floats: LPR lanes per row (power of two), each
+// lane owning CPL groups of 4 consecutive columns, 64/LPR rows per wavefront.
+struct RowGeom {
+  int lpr;
+  int cpl;
+};
+
+inline RowGeom row_geom(int dim) {
+  const int e4 = dim / 4;
+  int lpr = 1;
+  while (lpr < e4 && lpr < kWave) lpr *= 2;
+  const int cpl = (e4 + lpr - 1) / lpr;
+  return {lpr, cpl};
+}
+
+// Blocks are handed to the 8 XCDs round-robin (block b runs on XCD b % 8).
+// Remap so that each XCD receives one contiguous range of logical blocks:
+// neighbouring bags (the same table) then share one XCD's L2.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t n) {
+  const uint32_t xcd = b % kNumXcd, idx = b / kNumXcd;
+  const uint32_t q = n / kNumXcd, r = n % kNumXcd;
+  return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x % kWave; }
+
+__device__ __forceinline__ uint32_t key_of(uint64_t p) { return uint32_t(p >> 32); }
+__device__ __forceinline__ uint32_t bag_of(uint64_t p) { return uint32_t(p); }
+
+// ---- launchers (host) ------------------------------------------------------
+struct BwdLayout {
+  int64_t ns;
+  int64_t ntiles;      // radix tiles of kTile keys
+  int64_t nkeyblocks;  // blocks of the key-build kernel
+  int64_t chunk;       // sorted look-ups per segment-reduce chunk
+  int64_t nchunks;
+  int passes;          // radix passes
+  size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, total;
+};
+
+BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
+                          bool for_dedup);
+
+hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
+                          const int32_t* O, int64_t NS, float* Y, int32_t* status,
+                          hipStream_t st);
+
+// Builds keys, validates, sorts; returns the buffer holding the sorted pairs.
+hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
+                       int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
+                       hipStream_t st, uint64_t** sorted);
+
+hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
+                              float lr, const uint64_t* sorted, const BwdLayout& L, char* ws,
+                              hipStream_t st);
+
+hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
+                         uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,
+                         int32_t* seg_off, int32_t* d_num_unique, hipStream_t st);
+
+hipError_t launch_split(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t st);
+hipError_t launch_combine(const uint16_t* hi, const uint16_t* lo, float* w, int64_t n,
+                          hipStream_t st);
+
+}  // namespace embbag

@@ -1,0 +1,197 @@
+// Forward of the EmbeddingBag step (Algorithm 1, sum pooling) for gfx950.
+//
+// Each "row group" of LPR lanes owns G consecutive bags of one table and walks
+// their look-ups (contiguous in `indices`) as one list: U row loads are in
+// flight per lane before any of them is summed, and a bag's FP32 sum is
+// stored when the walk crosses the bag's end offset (empty bags store +0.0).
+// Every lane holds CPL groups of 4 columns, so a row is read with 128-bit
+// loads (64-bit for the BF16 halves of a split table).  Blocks are remapped
+// so that each XCD walks one contiguous range of bags: those bags belong to
+// one or two tables, whose hot rows then stay in that XCD's L2.
+#include "common.hpp"
+
+namespace embbag {
+namespace {
+
+template <bool SPLIT>
+__device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, int E, int col4) {
+  if constexpr (!SPLIT) {
+    const float* p = static_cast<const float*>(base) + size_t(row) * E + col4 * 4;
+    return *reinterpret_cast<const f4*>(p);
+  } else {
+    // BF16 high halves: element e is the 16 MSBs of an FP32 value.
+    const uint16_t* p = static_cast<const uint16_t*>(base) + size_t(row) * E + col4 * 4;
+    const u2 v = *reinterpret_cast<const u2*>(p);
+    f4 r;
+    r.x = __uint_as_float(v.x << 16);
+    r.y = __uint_as_float(v.x & 0xFFFF0000u);
+    r.z = __uint_as_float(v.y << 16);
+    r.w = __uint_as_float(v.y & 0xFFFF0000u);
+    return r;
+  }
+}
+
+template <int LPR, int CPL, bool SPLIT>
+__global__ __launch_bounds__(kBlock) void fwd_gather_sum(
+    TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
+    int32_t B, int32_t G, int32_t groups_per_table, int32_t items, float* __restrict__ Y,
+    int32_t* __restrict__ status) {
+  constexpr int R = kWave / LPR;
+  constexpr int U = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
+  const int E = d.dim;
+  const int E4 = E / 4;
+  const int lane = lane_id();
+  const int rg = lane / LPR, rl = lane % LPR;
+  const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
+  const int item = (blk * kWavesPerBlock + wave_id()) * R + rg;
+  if (item >= items) return;
+
+  const int TB = d.num_tables * B;
+  const int t = item / groups_per_table;
+  const int k0 = t * B + (item - t * groups_per_table) * G;
+  const int k1 = min(k0 + G, (t + 1) * B);
+  const uint32_t M = d.rows[t];
+  const void* base = d.w[t];
+  int err = 0;
+
+  auto store_bag = [&](int k, const f4* acc) {
+    float* y = Y + size_t(k) * E;
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c4 = rl + j * LPR;
+      if (c4 < E4) *reinterpret_cast<f4*>(y + c4 * 4) = acc[j];
+    }
+  };
+
+  const int s0 = O[k0], s1 = O[k1];
+  if ((k0 == 0 && s0 != 0) || (k1 == TB && s1 != NS)) err = EMBBAG_ERR_OFFSETS;
+  bool bad = s0 < 0 || s1 > NS || s0 > s1;
+  int k = k0;
+  int bound = bad ? 0 : O[k0 + 1];
+  bad = bad || bound < s0 || bound > s1;
+
+  f4 acc[CPL];
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  for (int s = s0; s < s1 && !bad; s += U) {
+    f4 v[U][CPL];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ss = s + u;
+      const int idx = ss < s1 ? I[ss] : 0;
+      const bool ok = ss < s1 && uint32_t(idx) < M;
+      if (ss < s1 && !ok) err = min(err, EMBBAG_ERR_INDEX_RANGE);
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int c4 = rl + j * LPR;
+        v[u][j] = (ok && c4 < E4) ? load_row4<SPLIT>(base, uint32_t(idx), E, c4)
+                                  : f4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ss = s + u;
+      if (ss >= s1 || bad) break;
+      // Crossing the end of bag k (and of any empty bags after it).  While
+      // ss < s1 = O[k1] and O is non-decreasing up to s1, k + 1 < k1 here.
+      while (ss >= bound) {
+        store_bag(k, acc);
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+        ++k;
+        const int nb = O[k + 1];
+        if (nb < bound || nb > s1) {
+          bad = true;
+          break;
+        }
+        bound = nb;
+      }
+      if (bad) break;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) acc[j] += v[u][j];
+    }
+  }
+  if (!bad) {
+    store_bag(k, acc);
+    // Remaining bags of the group hold no look-ups: O[k'] == s1 for them all.
+    for (int kk = k + 1; kk < k1; ++kk) {
+      if (O[kk] != s1) bad = true;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+      store_bag(kk, acc);
+    }
+  }
+  if (bad) err = EMBBAG_ERR_OFFSETS;
+  if (err != 0 && rl == 0 && status != nullptr) atomicMin(status, err);
+}
+
+// T*B == 0: the only data check left is offsets[0] == 0 == num_indices.
+__global__ void fwd_empty_check(const int32_t* __restrict__ O, int32_t NS,
+                                int32_t* __restrict__ status) {
+  if (threadIdx.x == 0 && status != nullptr && (O[0] != 0 || NS != 0))
+    atomicMin(status, EMBBAG_ERR_OFFSETS);
+}
+
+template <bool SPLIT, int LPR, int CPL>
+void launch_one(dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I, const int32_t* O,
+                int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items, float* Y,
+                int32_t* status) {
+  hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT>), grid, dim3(kBlock), 0, st, d, I, O, NS,
+                     B, G, gpt, items, Y, status);
+}
+
+template <bool SPLIT>
+bool dispatch(RowGeom g, dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I,
+              const int32_t* O, int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items,
+              float* Y, int32_t* status) {
+#define EMB_FWD(L, C) launch_one<SPLIT, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status)
+  switch (g.lpr) {
+    case 1: EMB_FWD(1, 1); return true;
+    case 2: EMB_FWD(2, 1); return true;
+    case 4: EMB_FWD(4, 1); return true;
+    case 8: EMB_FWD(8, 1); return true;
+    case 16: EMB_FWD(16, 1); return true;
+    case 32: EMB_FWD(32, 1); return true;
+    case 64:
+      switch (g.cpl) {
+        case 1: EMB_FWD(64, 1); return true;
+        case 2: EMB_FWD(64, 2); return true;
+        case 3: EMB_FWD(64, 3); return true;
+        case 4: EMB_FWD(64, 4); return true;
+      }
+  }
+#undef EMB_FWD
+  return false;
+}
+
+}  // namespace
+
+hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
+                          const int32_t* O, int64_t NS, float* Y, int32_t* status,
+                          hipStream_t st) {
+  const int64_t TB = int64_t(d.num_tables) * B;
+  if (TB == 0) {
+    hipLaunchKernelGGL(fwd_empty_check, dim3(1), dim3(kWave), 0, st, O, int32_t(NS), status);
+    return hipGetLastError();
+  }
+  // Bags per row group: enough look-ups per group to keep ~16 row loads per
+  // lane in flight when bags are short (P = 1 for the MLPerf-style tables).
+  const int64_t avg = NS / TB;
+  int G = avg >= 16 ? 1 : int(16 / (avg > 0 ? avg : 1));
+  G = G > 64 ? 64 : G;
+  G = G > B ? B : G;
+  const int gpt = (B + G - 1) / G;
+  const int64_t items = int64_t(d.num_tables) * gpt;
+  const RowGeom g = row_geom(d.dim);
+  const int per_block = kWavesPerBlock * (kWave / g.lpr);
+  const dim3 grid(unsigned((items + per_block - 1) / per_block));
+  const bool ok = split ? dispatch<true>(g, grid, st, d, I, O, int32_t(NS), B, G, gpt,
+                                         int32_t(items), Y, status)
+                        : dispatch<false>(g, grid, st, d, I, O, int32_t(NS), B, G, gpt,
+                                          int32_t(items), Y, status);
+  if (!ok) return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace embbag

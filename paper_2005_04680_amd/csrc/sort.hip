@@ -1,0 +1,394 @@
+// Integer work of the backward on gfx950: bag ids, keys, validation, a stable
+// LSD radix sort of (key, bag) pairs, and (for the checking entry point) the
+// unique keys with their segment offsets.
+//
+// A look-up s of bag k (table t = k / B) gets key = rowbase[t] + indices[s];
+// it travels as one 64-bit word (key << 32 | k), so a stable sort on the key
+// bits alone keeps the look-ups of one row in increasing s.  The sort is
+// reduce-then-scan, one pass per 8-bit digit: a per-tile digit histogram, a
+// scan per digit over the tiles, and a scatter in which every 4096-key tile
+// is ranked in LDS (wavefront ballots give each lane its rank among equal
+// digits) and written out in digit order, so that the global stores form
+// runs of consecutive addresses.  No kernel waits on another workgroup.
+#include "common.hpp"
+
+namespace embbag {
+namespace {
+
+// Inclusive scan across a wavefront (64 lanes).
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t n = __shfl_up(v, off, kWave);
+    if (lane >= off) v += n;
+  }
+  return v;
+}
+
+// Exclusive scan of one value per thread over a 256-thread block; returns the
+// exclusive prefix and writes the block total to *total.  `scratch` holds
+// kWavesPerBlock + 1 words of LDS.  Every thread must call it.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scratch,
+                                                         uint32_t* total) {
+  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  const uint32_t inc = wave_inclusive_scan(v);
+  if (lane == kWave - 1) scratch[w] = inc;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) {
+    const uint32_t s = scratch[i];
+    before += i < w ? s : 0u;
+    all += s;
+  }
+  __syncthreads();
+  *total = all;
+  return before + inc - v;
+}
+
+// Bags, keys and the first digit's histogram for one tile; offsets checks for
+// a slice of the bags; one status word per block.
+__global__ __launch_bounds__(kBlock) void build_keys(
+    TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
+    int32_t B, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
+    uint32_t* __restrict__ hist, int32_t* __restrict__ parts) {
+  __shared__ uint32_t lbag[kTile];
+  __shared__ uint32_t lhist[kRadix];
+  __shared__ int32_t lerr;
+  __shared__ int32_t krange[2];
+  const int tid = threadIdx.x;
+  const int blk = blockIdx.x;
+  int err = 0;
+  if (tid == 0) lerr = 0;
+  lhist[tid] = 0;
+  __syncthreads();
+
+  // Offsets: O[0] == 0, O non-decreasing, O[TB] == NS, all within [0, NS].
+  const int kb0 = blk * vb, kb1 = min(kb0 + vb, TB + 1);
+  for (int k = kb0 + tid; k < kb1; k += kBlock) {
+    const int o = O[k];
+    if (o < 0 || o > NS || (k == 0 && o != 0) || (k == TB && o != NS)) err = EMBBAG_ERR_OFFSETS;
+    if (k < TB && O[k + 1] < o) err = EMBBAG_ERR_OFFSETS;
+  }
+
+  const int s_lo = blk * kTile;
+  const int s_hi = min(s_lo + kTile, NS);
+  if (s_lo < s_hi) {  // uniform over the block
+    for (int i = tid; i < kTile; i += kBlock) lbag[i] = 0;
+    if (tid < 2) {
+      // last bag k in [0, TB - 1] with O[k] <= x (binary search; O monotone
+      // when valid, and clamped so a bad O still stays in bounds)
+      const int x = tid == 0 ? s_lo : s_hi - 1;
+      int lo = 0, hi = TB - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (O[mid] <= x) lo = mid; else hi = mid - 1;
+      }
+      krange[tid] = lo;
+    }
+    __syncthreads();
+    // Expand bag ids over the tile's look-ups.
+    for (int k = krange[0] + tid; k <= krange[1]; k += kBlock) {
+      const int a = max(O[k], s_lo), b = min(O[k + 1], s_hi);
+      for (int s = a; s < b; ++s) lbag[s - s_lo] = uint32_t(k);
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int i = 0; i < kItemsPerThread; ++i) {
+      const int s = s_lo + i * kBlock + tid;
+      if (s < s_hi) {
+        const uint32_t k = min(lbag[s - s_lo], uint32_t(TB - 1));
+        const uint32_t t = k / uint32_t(B);
+        int32_t r = I[s];
+        if (uint32_t(r) >= d.rows[t]) {
+          err = min(err, EMBBAG_ERR_INDEX_RANGE);
+          r = 0;
+        }
+        const uint32_t key = d.rowbase[t] + uint32_t(r);
+        out[s] = (uint64_t(key) << 32) | k;
+        atomicAdd(&lhist[key & (kRadix - 1)], 1u);
+      }
+    }
+    __syncthreads();
+    hist[size_t(tid) * ntiles + blk] = lhist[tid];
+  }
+  if (err != 0) atomicMin(&lerr, err);
+  __syncthreads();
+  if (tid == 0) parts[blk] = lerr;
+}
+
+// Digit histogram of one tile of the current arrangement.
+__global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restrict__ src,
+                                                        int32_t NS, int shift, int32_t ntiles,
+                                                        uint32_t* __restrict__ hist) {
+  __shared__ uint32_t lhist[kRadix];
+  const int tid = threadIdx.x, blk = blockIdx.x;
+  lhist[tid] = 0;
+  __syncthreads();
+  const int base = blk * kTile;
+#pragma unroll 4
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    const int s = base + i * kBlock + tid;
+    if (s < NS) atomicAdd(&lhist[(key_of(src[s]) >> shift) & (kRadix - 1)], 1u);
+  }
+  __syncthreads();
+  hist[size_t(tid) * ntiles + blk] = lhist[tid];
+}
+
+// Block d < 256: exclusive scan of digit d's tile counts (in tile order) and
+// the digit total.  Block 256 (first pass only): folds the per-block status
+// words into this call's verdict and lowers the caller's status word.
+__global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist, int32_t ntiles,
+                                                     uint32_t* __restrict__ totals,
+                                                     const int32_t* __restrict__ parts,
+                                                     int32_t nparts, int32_t* __restrict__ flags,
+                                                     int32_t* __restrict__ d_status) {
+  __shared__ uint32_t scratch[kWavesPerBlock + 1];
+  __shared__ int32_t lerr;
+  const int tid = threadIdx.x;
+  if (blockIdx.x == kRadix) {
+    if (tid == 0) lerr = 0;
+    __syncthreads();
+    int e = 0;
+    for (int i = tid; i < nparts; i += kBlock) e = min(e, parts[i]);
+    if (e != 0) atomicMin(&lerr, e);
+    __syncthreads();
+    if (tid == 0) {
+      flags[0] = lerr;
+      if (lerr != 0 && d_status != nullptr) atomicMin(d_status, lerr);
+    }
+    return;
+  }
+  uint32_t* row = hist + size_t(blockIdx.x) * ntiles;
+  uint32_t running = 0;
+  for (int base = 0; base < ntiles; base += kBlock) {
+    const int i = base + tid;
+    const uint32_t v = i < ntiles ? row[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(v, scratch, &tot);
+    if (i < ntiles) row[i] = running + ex;
+    running += tot;
+  }
+  if (tid == 0) totals[blockIdx.x] = running;
+}
+
+// Stable scatter of one tile by the digit at `shift`.
+__global__ __launch_bounds__(kBlock) void radix_downsweep(
+    const uint64_t* __restrict__ src, uint64_t* __restrict__ dst, int32_t NS, int shift,
+    int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals) {
+  __shared__ uint64_t buf[kTile];
+  __shared__ uint32_t whist[kWavesPerBlock][kRadix];
+  __shared__ uint32_t lstart[kRadix];
+  __shared__ uint32_t gbase[kRadix];
+  __shared__ uint32_t scratch[kWavesPerBlock + 1];
+  const int tid = threadIdx.x, blk = blockIdx.x;
+  const int lane = lane_id();
+  const int w = tid / kWave;
+
+  // Global start of each digit's run for this tile.
+  {
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(totals[tid], scratch, &tot);
+    gbase[tid] = ex + hist[size_t(tid) * ntiles + blk];
+  }
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) whist[i][tid] = 0;
+  __syncthreads();
+
+  // Wave w owns keys [w*1024, (w+1)*1024) of the tile, item i of lane l being
+  // key w*1024 + i*64 + l: ranking item by item keeps the original order.
+  const int wbase = blk * kTile + w * (kWave * kItemsPerThread);
+  uint64_t item[kItemsPerThread];
+  uint32_t dig[kItemsPerThread];
+  uint32_t rank[kItemsPerThread];
+#pragma unroll
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    const int pos = wbase + i * kWave + lane;
+    item[i] = pos < NS ? src[pos] : ~0ull;
+  }
+  const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    const bool valid = wbase + i * kWave + lane < NS;
+    const uint32_t dg = (key_of(item[i]) >> shift) & (kRadix - 1);
+    dig[i] = dg;
+    uint64_t peers = __builtin_amdgcn_ballot_w64(valid);
+#pragma unroll
+    for (int b = 0; b < kRadixBits; ++b) {
+      const bool bit = (dg >> b) & 1u;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(bit);
+      peers &= bit ? m : ~m;
+    }
+    const uint32_t lrank = uint32_t(__popcll(peers & below));
+    const uint32_t cnt = uint32_t(__popcll(peers));
+    const uint32_t prior = whist[w][dg];
+    rank[i] = prior + lrank;
+    if (valid && lrank == 0) whist[w][dg] = prior + cnt;
+  }
+  __syncthreads();
+  {
+    // Per digit: offsets of each wave's run inside the tile's digit run, and
+    // the start of each digit's run in the locally sorted tile.
+    uint32_t run = 0;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+      const uint32_t c = whist[i][tid];
+      whist[i][tid] = run;
+      run += c;
+    }
+    uint32_t tot;
+    lstart[tid] = block_exclusive_scan(run, scratch, &tot);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    if (wbase + i * kWave + lane < NS) buf[lstart[dig[i]] + whist[w][dig[i]] + rank[i]] = item[i];
+  }
+  __syncthreads();
+  const int nvalid = min(kTile, NS - blk * kTile);
+  for (int j = tid; j < nvalid; j += kBlock) {
+    const uint64_t it = buf[j];
+    const uint32_t dg = (key_of(it) >> shift) & (kRadix - 1);
+    dst[gbase[dg] + (j - lstart[dg])] = it;
+  }
+}
+
+// ---- unique keys and segment offsets (checking entry point only) ----------
+
+// Unpacks one tile and counts its segment heads.
+__global__ __launch_bounds__(kBlock) void unique_count(const uint64_t* __restrict__ sorted,
+                                                       int32_t NS, uint32_t* __restrict__ skeys,
+                                                       uint32_t* __restrict__ sbags,
+                                                       uint32_t* __restrict__ counts) {
+  __shared__ uint32_t scratch[kWavesPerBlock + 1];
+  const int tid = threadIdx.x, blk = blockIdx.x;
+  uint32_t c = 0;
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    const int s = blk * kTile + i * kBlock + tid;
+    if (s < NS) {
+      const uint64_t p = sorted[s];
+      skeys[s] = key_of(p);
+      sbags[s] = bag_of(p);
+      c += (s == 0 || key_of(sorted[s - 1]) != key_of(p)) ? 1u : 0u;
+    }
+  }
+  uint32_t tot;
+  block_exclusive_scan(c, scratch, &tot);
+  if (tid == 0) counts[blk] = tot;
+}
+
+// Exclusive scan of the per-tile head counts (one block); writes U and seg_off[U].
+__global__ __launch_bounds__(kBlock) void unique_scan(uint32_t* __restrict__ counts,
+                                                      int32_t ntiles, int32_t NS,
+                                                      int32_t* __restrict__ seg_off,
+                                                      int32_t* __restrict__ d_num_unique) {
+  __shared__ uint32_t scratch[kWavesPerBlock + 1];
+  const int tid = threadIdx.x;
+  uint32_t running = 0;
+  for (int base = 0; base < ntiles; base += kBlock) {
+    const int i = base + tid;
+    const uint32_t v = i < ntiles ? counts[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(v, scratch, &tot);
+    if (i < ntiles) counts[i] = running + ex;
+    running += tot;
+  }
+  if (tid == 0) {
+    *d_num_unique = int32_t(running);
+    seg_off[running] = NS;
+  }
+}
+
+// Writes unique_keys[u] and seg_off[u] for the heads of one tile, in order.
+__global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restrict__ sorted,
+                                                       int32_t NS,
+                                                       const uint32_t* __restrict__ tile_off,
+                                                       uint32_t* __restrict__ ukeys,
+                                                       int32_t* __restrict__ seg_off) {
+  __shared__ uint32_t scratch[kWavesPerBlock + 1];
+  const int tid = threadIdx.x, blk = blockIdx.x;
+  uint32_t running = tile_off[blk];
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    const int s = blk * kTile + i * kBlock + tid;
+    bool head = false;
+    uint32_t key = 0;
+    if (s < NS) {
+      key = key_of(sorted[s]);
+      head = s == 0 || key_of(sorted[s - 1]) != key;
+    }
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(head ? 1u : 0u, scratch, &tot);
+    if (head) {
+      ukeys[running + ex] = key;
+      seg_off[running + ex] = s;
+    }
+    running += tot;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
+                       int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
+                       hipStream_t st, uint64_t** sorted) {
+  const int32_t TB = d.num_tables * B;
+  uint64_t* a = reinterpret_cast<uint64_t*>(ws + L.off_a);
+  uint64_t* b = reinterpret_cast<uint64_t*>(ws + L.off_b);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.off_hist);
+  uint32_t* totals = reinterpret_cast<uint32_t*>(ws + L.off_tot);
+  int32_t* parts = reinterpret_cast<int32_t*>(ws + L.off_parts);
+  int32_t* flags = reinterpret_cast<int32_t*>(ws + L.off_flags);
+  const int nkb = int(L.nkeyblocks);
+  const int vb = (TB + 1 + nkb - 1) / nkb;
+  const int ntiles = int(L.ntiles);
+  hipLaunchKernelGGL(build_keys, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B, TB,
+                     ntiles, vb, a, hist, parts);
+  // Status verdict (block 256 of the first scan, or alone when nothing is sorted).
+  const int passes = NS > 0 ? L.passes : 0;
+  if (passes == 0) {
+    hipLaunchKernelGGL(radix_scan, dim3(kRadix + 1), dim3(kBlock), 0, st, hist, 0, totals, parts,
+                       nkb, flags, d_status);
+    *sorted = a;
+    return hipGetLastError();
+  }
+  uint64_t* src = a;
+  uint64_t* dst = b;
+  for (int p = 0; p < passes; ++p) {
+    const int shift = p * kRadixBits;
+    if (p > 0)
+      hipLaunchKernelGGL(radix_upsweep, dim3(ntiles), dim3(kBlock), 0, st, src, int32_t(NS),
+                         shift, ntiles, hist);
+    hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? kRadix + 1 : kRadix), dim3(kBlock), 0, st, hist,
+                       ntiles, totals, parts, nkb, flags, d_status);
+    hipLaunchKernelGGL(radix_downsweep, dim3(ntiles), dim3(kBlock), 0, st, src, dst,
+                       int32_t(NS), shift, ntiles, hist, totals);
+    uint64_t* tmp = src;
+    src = dst;
+    dst = tmp;
+  }
+  *sorted = src;
+  return hipGetLastError();
+}
+
+hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
+                         uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,
+                         int32_t* seg_off, int32_t* d_num_unique, hipStream_t st) {
+  uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.off_uniq);
+  const int ntiles = int(L.ntiles);
+  if (L.ns == 0) {
+    hipLaunchKernelGGL(unique_scan, dim3(1), dim3(kBlock), 0, st, counts, 0, 0, seg_off,
+                       d_num_unique);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(unique_count, dim3(ntiles), dim3(kBlock), 0, st, sorted, int32_t(L.ns),
+                     sorted_keys, sorted_bags, counts);
+  hipLaunchKernelGGL(unique_scan, dim3(1), dim3(kBlock), 0, st, counts, ntiles, int32_t(L.ns),
+                     seg_off, d_num_unique);
+  hipLaunchKernelGGL(unique_write, dim3(ntiles), dim3(kBlock), 0, st, sorted, int32_t(L.ns),
+                     counts, unique_keys, seg_off);
+  return hipGetLastError();
+}
+
+}  // namespace embbag

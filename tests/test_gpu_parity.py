@@ -1,0 +1,279 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Floating point: |gpu - oracle| <= 1e-6 + 1e-5 |oracle| elementwise for pooled
+outputs and updated rows; rows no look-up names must keep their bits.
+Integer work (sorted keys/bags, unique keys, segment offsets, U): bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from embbag_data import get_config, make_batch, make_grads, random_bags, scaled, table_values_np
+from gpu_util import (DEV, GpuTables, assert_close, bits_equal, gpu_dedup, log, require_gpu,
+                      to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _tables(rng, rows, dim, scale):
+    return [rng.uniform(-scale, scale, size=(m, dim)).astype(np.float32) for m in rows]
+
+
+def check_step(W, batch, I, O, G, lr, split=False, what=""):
+    """Forward + fused backward on the GPU vs the oracle; returns GPU tables."""
+    log(f"[parity] {what} T={len(W)} E={W[0].shape[1]} B={batch} NS={I.size} split={split}")
+    gt = GpuTables(W, split=split)
+    rc, Y = gt.forward(batch, I, O)
+    assert rc == 0
+    if split:
+        his = [oracle.split(w)[0] for w in W]
+        orc, Yref = oracle.forward_split(his, batch, I, O)
+    else:
+        orc, Yref = oracle.forward(W, batch, I, O)
+    assert orc == 0
+    assert_close(Y.cpu().numpy(), Yref, f"{what} pooled")
+    assert gt.backward(G, batch, I, O, lr) == 0
+    assert gt.read_status() == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd(G, batch, I, O, lr, Wref) == 0
+    Wg = gt.host()
+    for t in range(len(W)):
+        lo_, hi_ = O[t * batch], O[(t + 1) * batch]
+        touched = np.zeros(W[t].shape[0], bool)
+        touched[I[lo_:hi_]] = True
+        assert_close(Wg[t][touched], Wref[t][touched], f"{what} table {t} touched rows")
+        assert bits_equal(Wg[t][~touched], W[t][~touched]), f"{what} table {t} untouched rows changed"
+    return gt
+
+
+# ---------------------------------------------------------------------------
+# Tiny workload (4 x 1000 x 16, B=32, P=4)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("batch_id", [0, 1])
+def test_tiny(batch_id):
+    cfg = get_config("tiny")
+    W = [table_values_np(cfg.seed, t, np.arange(cfg.rows[t]), cfg.dim, cfg.value_scale[t])
+         for t in range(cfg.num_tables)]
+    I, O = make_batch(cfg, batch_id)
+    G = make_grads(cfg, batch_id)
+    check_step(W, cfg.batch, I, O, G, cfg.lr, what=f"tiny/{batch_id}")
+
+
+# ---------------------------------------------------------------------------
+# Every row geometry (lanes per row x column groups per lane), variable bags,
+# empty bags, duplicate-heavy rows, ragged tails
+# ---------------------------------------------------------------------------
+DIMS = [4, 8, 12, 16, 20, 32, 64, 100, 128, 256, 260, 512, 768, 1024]
+
+
+@pytest.mark.parametrize("dim", DIMS)
+def test_row_geometries(dim):
+    rng = np.random.default_rng(1000 + dim)
+    rows = (300, 57, 1000)
+    W = _tables(rng, rows, dim, 0.05)
+    I, O = random_bags(rng, rows, 37, 20, empty_frac=0.15, hot_frac=0.2)
+    G = rng.standard_normal((len(rows), 37, dim)).astype(np.float32)
+    check_step(W, 37, I, O, G, 0.1, what=f"dim{dim}")
+
+
+@pytest.mark.parametrize("dim", [16, 64, 256])
+def test_row_geometries_split(dim):
+    rng = np.random.default_rng(2000 + dim)
+    rows = (500, 77)
+    W = _tables(rng, rows, dim, 0.05)
+    I, O = random_bags(rng, rows, 29, 12, empty_frac=0.1, hot_frac=0.3)
+    G = rng.standard_normal((len(rows), 29, dim)).astype(np.float32)
+    check_step(W, 29, I, O, G, 0.1, split=True, what=f"split dim{dim}")
+
+
+@pytest.mark.parametrize("pool,batch,hot", [(1, 5000, 0.5), (3, 3001, 0.0), (50, 700, 0.3),
+                                            (200, 64, 0.6)])
+def test_many_tiles_and_long_segments(pool, batch, hot):
+    """NS spans many radix tiles and segment chunks; hot rows make segments that
+    cross hundreds of chunks; bag sizes and the tail are ragged."""
+    rng = np.random.default_rng(pool * 7 + batch)
+    rows = (20000, 3, 5000)
+    dim = 64
+    W = _tables(rng, rows, dim, 0.01)
+    I, O = random_bags(rng, rows, batch, pool, empty_frac=0.05, hot_frac=hot)
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    check_step(W, batch, I, O, G, 0.1, what=f"tiles P<={pool}")
+
+
+def test_small_full():
+    """Small-shaped workload at full size: 8 x 1e6 x 64, B=2048, P=32, Zipf(1.05)."""
+    cfg = get_config("small")
+    W = [table_values_np(cfg.seed, t, np.arange(cfg.rows[t]), cfg.dim, cfg.value_scale[t])
+         for t in range(cfg.num_tables)]
+    I, O = make_batch(cfg, 0)
+    G = make_grads(cfg, 0)
+    check_step(W, cfg.batch, I, O, G, cfg.lr, what="small")
+
+
+def test_split_full():
+    """Split-SGD-BF16 workload: Small-shaped tables stored as hi/lo halves."""
+    cfg = get_config("split")
+    W = [table_values_np(cfg.seed, t, np.arange(cfg.rows[t]), cfg.dim, cfg.value_scale[t])
+         for t in range(cfg.num_tables)]
+    I, O = make_batch(cfg, 0)
+    G = make_grads(cfg, 0)
+    check_step(W, cfg.batch, I, O, G, cfg.lr, split=True, what="split")
+
+
+# ---------------------------------------------------------------------------
+# Integer work: bit-exact
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("case", ["tiny", "random", "p1_hot", "small", "mlperf_scaled"])
+def test_dedup_bit_exact(case):
+    rng = np.random.default_rng(5)
+    if case == "tiny":
+        cfg = get_config("tiny")
+        rows, batch = cfg.rows, cfg.batch
+        I, O = make_batch(cfg, 0)
+    elif case == "random":
+        rows, batch = (1000, 5, 70000), 900
+        I, O = random_bags(rng, rows, batch, 30, 0.1, 0.2)
+    elif case == "p1_hot":
+        rows, batch = (10, 1000000), 50000
+        I, O = random_bags(rng, rows, batch, 1, 0.0, 0.4)
+    elif case == "small":
+        cfg = get_config("small")
+        rows, batch = cfg.rows, cfg.batch
+        I, O = make_batch(cfg, 1)
+    else:
+        cfg = scaled(get_config("mlperf"), batch=8192)
+        rows, batch = cfg.rows, cfg.batch
+        I, O = make_batch(cfg, 0)
+    log(f"[dedup] {case} NS={I.size}")
+    rc, d_ref = oracle.dedup(rows, batch, I, O)
+    assert rc == 0
+    rc, status, d = gpu_dedup(rows, batch, I, O)
+    assert rc == 0 and status == 0
+    assert d["num_unique"] == d_ref["num_unique"]
+    for k in ("sorted_keys", "sorted_bags", "unique_keys", "seg_off"):
+        assert np.array_equal(d[k], d_ref[k]), k
+
+
+# ---------------------------------------------------------------------------
+# Invariants, determinism, edge cases, errors
+# ---------------------------------------------------------------------------
+def test_lr_zero_and_determinism():
+    rng = np.random.default_rng(9)
+    rows = (4000, 4000)
+    W = _tables(rng, rows, 128, 0.1)
+    I, O = random_bags(rng, rows, 500, 40, 0.05, 0.3)
+    G = rng.standard_normal((2, 500, 128)).astype(np.float32)
+    g0 = GpuTables(W)
+    assert g0.backward(G, 500, I, O, 0.0) == 0
+    for a, b in zip(g0.host(), W):
+        assert bits_equal(a, b)
+    ga, gb = GpuTables(W), GpuTables(W)
+    assert ga.backward(G, 500, I, O, 0.1) == 0
+    assert gb.backward(G, 500, I, O, 0.1) == 0
+    for a, b in zip(ga.host(), gb.host()):
+        assert bits_equal(a, b)
+    _, Ya = ga.forward(500, I, O)
+    _, Yb = gb.forward(500, I, O)
+    assert bits_equal(Ya.cpu().numpy(), Yb.cpu().numpy())
+
+
+def test_exact_special_cases():
+    rng = np.random.default_rng(10)
+    W = _tables(rng, (50,), 64, 1.0)
+    I = np.array([7, 9, 9], np.int32)
+    O = np.array([0, 1, 3, 3], np.int32)
+    gt = GpuTables(W)
+    rc, Y = gt.forward(3, I, O)
+    Y = Y.cpu().numpy()
+    assert bits_equal(Y[0, 0], W[0][7])              # single look-up = row copy
+    assert np.array_equal(Y[0, 1], 2 * W[0][9])      # [r, r] = 2 W[r]
+    assert bits_equal(Y[0, 2], np.zeros(64, np.float32))  # empty bag = +0.0
+
+
+def test_empty_inputs():
+    W = [np.ones((10, 16), np.float32)]
+    gt = GpuTables(W)
+    I = np.zeros(0, np.int32)
+    O = np.zeros(6, np.int32)
+    rc, Y = gt.forward(5, I, O)
+    assert rc == 0 and bits_equal(Y.cpu().numpy(), np.zeros((1, 5, 16), np.float32))
+    G = np.ones((1, 5, 16), np.float32)
+    assert gt.backward(G, 5, I, O, 0.1) == 0
+    assert gt.read_status() == 0
+    assert bits_equal(gt.host()[0], W[0])
+    # B = 0
+    rc, _ = gt.forward(0, I, np.zeros(1, np.int32))
+    assert rc == 0 and gt.read_status() == 0
+
+
+def test_index_out_of_range_is_reported_and_writes_nothing():
+    rng = np.random.default_rng(11)
+    rows = (100, 20)
+    W = _tables(rng, rows, 32, 0.1)
+    I, O = random_bags(rng, rows, 50, 10, 0.0, 0.0)
+    I[O[60] + 1] = 20           # a bag of table 1, row 20 of 20
+    G = rng.standard_normal((2, 50, 32)).astype(np.float32)
+    assert oracle.validate(rows, 32, 50, I, O) == oracle.ERR_INDEX_RANGE
+    gt = GpuTables(W)
+    rc, _ = gt.forward(50, I, O)
+    assert rc == 0 and gt.read_status() == oracle.ERR_INDEX_RANGE
+    gt.reset_status()
+    assert gt.backward(G, 50, I, O, 0.1) == 0
+    assert gt.read_status() == oracle.ERR_INDEX_RANGE
+    for a, b in zip(gt.host(), W):
+        assert bits_equal(a, b)
+    I[5] = -3
+    gt.reset_status()
+    assert gt.backward(G, 50, I, O, 0.1) == 0
+    assert gt.read_status() == oracle.ERR_INDEX_RANGE
+
+
+@pytest.mark.parametrize("kind", ["first", "decreasing", "last", "both"])
+def test_bad_offsets_are_reported_and_write_nothing(kind):
+    rng = np.random.default_rng(12)
+    rows = (100, 20)
+    W = _tables(rng, rows, 16, 0.1)
+    I, O = random_bags(rng, rows, 40, 10, 0.0, 0.0)
+    G = rng.standard_normal((2, 40, 16)).astype(np.float32)
+    O = O.copy()
+    if kind == "first":
+        O[0] = 1
+    elif kind == "decreasing":
+        O[30] = O[31] + 1
+    elif kind == "last":
+        O[-1] -= 1
+    else:
+        O[30] = O[31] + 1
+        I[0] = 100
+    assert oracle.validate(rows, 16, 40, I, O) == oracle.ERR_OFFSETS
+    gt = GpuTables(W)
+    rc, _ = gt.forward(40, I, O)
+    assert rc == 0 and gt.read_status() == oracle.ERR_OFFSETS
+    gt.reset_status()
+    assert gt.backward(G, 40, I, O, 0.1) == 0
+    assert gt.read_status() == oracle.ERR_OFFSETS
+    for a, b in zip(gt.host(), W):
+        assert bits_equal(a, b)
+
+
+def test_split_helpers_bit_exact():
+    import paper_2005_04680_amd as pk
+    rng = np.random.default_rng(13)
+    w = np.concatenate([rng.standard_normal(1 << 20).astype(np.float32),
+                        rng.integers(0, 2 ** 32, 4099, dtype=np.uint64).astype(np.uint32).view(np.float32)])
+    hi_ref, lo_ref = oracle.split(w)
+    wd = to_dev(w)
+    hi = torch.empty(w.size, dtype=torch.int16, device=DEV)
+    lo = torch.empty(w.size, dtype=torch.int16, device=DEV)
+    assert pk.embbag_split_fp32(wd, hi, lo) == 0
+    assert np.array_equal(hi.cpu().numpy().view(np.uint16), hi_ref)
+    assert np.array_equal(lo.cpu().numpy().view(np.uint16), lo_ref)
+    back = torch.empty_like(wd)
+    assert pk.embbag_combine_fp32(hi, lo, back) == 0
+    assert bits_equal(back.cpu().numpy(), w)
