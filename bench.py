@@ -1,0 +1,332 @@
+#!/usr/bin/env python3
+"""Benchmark of the EmbeddingBag training step on one MI355X.
+
+A step is one pass of the whole hot path over one batch: the sum-pooled
+forward (Algorithm 1) followed by the backward fused with the sparse SGD
+update (Algorithms 2-3), on synthetic seeded data with inputs resident in
+HBM.  Default workload: the Large-shaped tables (16 x 6e6 rows x E=256 FP32,
+98.3 GB), batch 8192, 100 look-ups per bag, Zipf(1.05) indices, lr 0.1,
+rotating over pre-generated batches.
+
+Prints ONE JSON line: lookups/s (value), algorithmic HBM GB/s and % of the
+8 TB/s peak for the whole step, the roofline record of the dominant kernel
+(timed with HIP events on the launch stream), and the CPU oracle timed on a
+bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "embedding lookups/sec and achieved HBM GB/s (fwd+bwd+update), % of HBM peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def describe(cfg):
+    if cfg.name == "mlperf":
+        return (f"mlperf: 26 tables, log-uniform rows in [10, 4e7] ({cfg.table_bytes / 1e9:.1f} GB FP32), "
+                f"E=128, batch 65536, 1 look-up/bag, Zipf(1.2)")
+    kind = "split-BF16 hi/lo" if cfg.split else "FP32"
+    dist = f"Zipf({cfg.zipf_s})" if cfg.dist == "zipf" else "uniform"
+    return (f"{cfg.name}: {cfg.num_tables} tables x {cfg.rows[0]:.0e} rows x E={cfg.dim} {kind} "
+            f"({cfg.table_bytes / 1e9:.1f} GB), batch {cfg.batch}, {cfg.pooling} look-ups/bag, {dist}")
+
+
+def bytes_model(cfg, U, split):
+    """Algorithmic HBM bytes of one step (forward, backward+update)."""
+    T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
+    TB = T * B
+    sw = 2 if split else 4
+    fwd = NS * E * sw + 4 * NS + 4 * (TB + 1) + 4 * TB * E
+    bwd = 4 * TB * E + 4 * NS + 4 * (TB + 1) + 2 * U * E * 4
+    return fwd, bwd
+
+
+def profiled_traffic(cfg, kernels):
+    """HBM-side bytes per launch of `kernels` from profiles/traffic.json (copy-calibrated
+    rocprofv3 FETCH_SIZE + WRITE_SIZE), or None when that record is for another
+    workload or the kernels' sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("workload") != cfg.name:
+        return None
+    total = 0
+    for k in kernels:
+        r = rec["kernels"].get(k)
+        if r is None:
+            return None
+        h = hashlib.sha256()
+        for src in r["sources"]:
+            h.update(open(os.path.join(ROOT, src), "rb").read())
+        if h.hexdigest() != r["source_sha256"]:
+            return None
+        total += r["fetch_bytes"] + r["write_bytes"]
+    return total
+
+
+def unique_count(cfg, I):
+    """Touched (table, row) pairs of one batch (plain numpy on the host)."""
+    n_t = cfg.batch * cfg.pooling
+    return int(sum(np.unique(I[t * n_t:(t + 1) * n_t]).size for t in range(cfg.num_tables)))
+
+
+def cpu_baseline(cfg, batch_I, G, sample_bags):
+    """The CPU oracle on the first `sample_bags` bags of every table of batch 0."""
+    import torch
+
+    import oracle
+    from embbag_data import table_rows_torch
+
+    P, B, T = cfg.pooling, cfg.batch, cfg.num_tables
+    nb = min(sample_bags, B)
+    I_s, tabs = [], []
+    for t in range(T):
+        part = batch_I[t * B * P: t * B * P + nb * P]
+        rows, inv = np.unique(part, return_inverse=True)
+        I_s.append(inv.astype(np.int32))
+        vals = table_rows_torch(cfg.seed, t, torch.from_numpy(rows).cuda(), cfg.dim,
+                                cfg.value_scale[t])
+        tabs.append(vals.cpu().numpy())
+    I_s = np.concatenate(I_s)
+    O_s = np.arange(0, T * nb * P + 1, P, dtype=np.int32)
+    G_s = np.ascontiguousarray(G[:, :nb, :])
+    if cfg.split:
+        his, los = zip(*[oracle.split(w) for w in tabs])
+        his, los = list(his), list(los)
+        t0 = time.perf_counter()
+        rc1, _ = oracle.forward_split(his, nb, I_s, O_s)
+        rc2 = oracle.backward_sgd_split(G_s, nb, I_s, O_s, cfg.lr, his, los)
+    else:
+        t0 = time.perf_counter()
+        rc1, _ = oracle.forward(tabs, nb, I_s, O_s)
+        rc2 = oracle.backward_sgd(G_s, nb, I_s, O_s, cfg.lr, tabs)
+    dt = time.perf_counter() - t0
+    assert rc1 == 0 and rc2 == 0
+    return {"value": I_s.size / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": (f"first {nb} of {B} bags of each of the {T} tables of batch 0 "
+                       f"({I_s.size} look-ups, {sum(x.shape[0] for x in tabs)} touched rows), "
+                       f"forward + fused backward/SGD, single-threaded, {dt:.2f} s")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="large",
+                    choices=["tiny", "small", "large", "mlperf", "split", "small_p50_uniform",
+                             "large_uniform"])
+    ap.add_argument("--batches", type=int, default=4, help="pre-generated batches, rotated")
+    ap.add_argument("--cpu-sample-bags", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--overlap-prepare", action="store_true",
+                    help="run the backward's index phase on a second stream, overlapped with "
+                         "the forward (measured slower on MI355X: both are memory-bound)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (the reference "
+                         "kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE to bytes)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(the tables shard table-wise across GPUs by design, "
+                                   "but no multi-GPU path is built)"}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2005_04680_amd as pk
+    from embbag_data import fill_table_torch, fill_tables_torch, get_config, make_batch, make_grads
+
+    pk.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.calibrate_copy:
+        n = 1 << 28  # 1 GiB of FP32
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read_per_copy": 4 * n,
+                          "bytes_written_per_copy": 4 * n, "copies": 5}), flush=True)
+        return
+    cfg = get_config(args.config)
+    T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
+    split = cfg.split
+
+    # ---- tables in HBM ----------------------------------------------------
+    t0 = time.time()
+    if split:
+        hi = [torch.empty((m, E), dtype=torch.int16, device=dev) for m in cfg.rows]
+        lo = [torch.empty((m, E), dtype=torch.int16, device=dev) for m in cfg.rows]
+        for t, m in enumerate(cfg.rows):
+            tmp = torch.empty((m, E), dtype=torch.float32, device=dev)
+            fill_table_torch(cfg, t, tmp)
+            pk.check(pk.embbag_split_fp32(tmp, hi[t], lo[t]), "split")
+            del tmp
+        tables = None
+    else:
+        tables = [torch.empty((m, E), dtype=torch.float32, device=dev) for m in cfg.rows]
+        fill_tables_torch(cfg, tables)
+    torch.cuda.synchronize()
+    log(f"[bench] tables filled ({cfg.table_bytes / 1e9:.1f} GB) in {time.time() - t0:.1f}s")
+
+    # ---- batches ----------------------------------------------------------
+    t0 = time.time()
+    batches = []
+    for b in range(args.batches):
+        I, O = make_batch(cfg, b, device=dev)
+        G = make_grads(cfg, b)
+        U = unique_count(cfg, I)
+        batches.append(dict(I=torch.from_numpy(I).to(dev), O=torch.from_numpy(O).to(dev),
+                            G=torch.from_numpy(G).to(dev), U=U, I_host=I if b == 0 else None,
+                            G_host=G if b == 0 else None))
+    log(f"[bench] {args.batches} batches generated in {time.time() - t0:.1f}s; "
+        f"U = {[x['U'] for x in batches]}")
+
+    Y = torch.empty((T, B, E), dtype=torch.float32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8, device=dev)
+
+    def fwd(bt):
+        if split:
+            return pk.embbag_forward_split_bf16(hi, B, bt["I"], bt["O"], Y, status)
+        return pk.embbag_forward(tables, B, bt["I"], bt["O"], Y, status)
+
+    def prep(bt):
+        return pk.embbag_backward_prepare(cfg.rows, E, B, bt["I"], bt["O"], ws, status)
+
+    def apply(bt):
+        if split:
+            return pk.embbag_backward_apply_sgd_split_bf16(bt["G"], B, NS, cfg.lr, hi, lo, ws)
+        return pk.embbag_backward_apply_sgd(bt["G"], B, NS, cfg.lr, tables, ws)
+
+    def bwd(bt):
+        rc = prep(bt)
+        return rc if rc else apply(bt)
+
+    for i in range(args.warmup):
+        bt = batches[i % len(batches)]
+        pk.check(fwd(bt), "forward")
+        pk.check(bwd(bt), "backward")
+    torch.cuda.synchronize()
+    pk.check(pk.embbag_status_read(status), "device status")
+
+    # ---- timed steps ------------------------------------------------------
+    # The backward's index phase (prepare) reads only indices and offsets, so
+    # with --overlap-prepare it runs on a second stream while the forward
+    # gathers rows; the apply phase waits for both, and the next step's
+    # prepare waits for this step's apply, which still reads the workspace.
+    K = args.steps
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream(device=dev) if args.overlap_prepare else main
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(6)) for _ in range(K)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(main)
+    prev_apply = start
+    for i in range(K):
+        bt = batches[i % len(batches)]
+        e_f0, e_f1, e_p0, e_p1, e_a0, e_a1 = ev[i]
+        side.wait_event(prev_apply)
+        with torch.cuda.stream(side):
+            e_p0.record(side)
+            prep(bt)
+            e_p1.record(side)
+        e_f0.record(main)
+        fwd(bt)
+        e_f1.record(main)
+        main.wait_event(e_p1)
+        e_a0.record(main)
+        apply(bt)
+        e_a1.record(main)
+        prev_apply = e_a1
+    stop.record(main)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    pk.check(pk.embbag_status_read(status), "device status")
+    total_ms = start.elapsed_time(stop)
+    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
+    prep_ms = sum(e[2].elapsed_time(e[3]) for e in ev) / K
+    apply_ms = sum(e[4].elapsed_time(e[5]) for e in ev) / K
+    ms_step = total_ms / K
+    U_avg = sum(batches[i % len(batches)]["U"] for i in range(K)) / K
+    fwd_b, bwd_b = bytes_model(cfg, U_avg, split)
+    step_b = fwd_b + bwd_b
+    gbps = step_b / (ms_step * 1e-3) / 1e9
+    # Roofline of the dominant kernel.  The forward call is one launch
+    # (fwd_gather_sum); the apply call is segment_sgd plus the short
+    # segment_fixup, whose events bracket both.  Algorithmic bytes per launch:
+    # forward = NS*E*s_w + 4*NS + 4*(TB+1) + 4*TB*E (every look-up reads its
+    # row); apply = dY once (4*TB*E) + the sorted look-ups (8*NS) + one read and
+    # one write of every touched row (2*U*E*s_row).
+    TB = T * B
+    apply_b = 4 * TB * E + 8 * NS + 2 * U_avg * E * 4
+    lpr = 64 if E >= 256 else max(1, 1 << max(0, (E // 4 - 1).bit_length()))
+    cpl = max(1, E // 4 // 64)
+    rows_t = "SplitRows" if split else "Fp32Rows"
+    if apply_ms >= fwd_ms:
+        roof_k, roof_b, roof_ms = "segment_sgd+segment_fixup", apply_b, apply_ms
+        kern = [f"segment_sgd<{lpr}, {cpl}, {rows_t}>", f"segment_fixup<{lpr}, {cpl}, {rows_t}>"]
+    else:
+        roof_k, roof_b, roof_ms = "fwd_gather_sum", fwd_b, fwd_ms
+        kern = [f"fwd_gather_sum<{lpr}, {cpl}, {'true' if split else 'false'}>"]
+    achieved = roof_b / (roof_ms * 1e-3) / 1e9
+    roof = {"kernel": roof_k, "bound": "hbm", "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": profiled_traffic(cfg, kern), "bytes_per_launch": int(roof_b),
+            "avg_launch_ms": round(roof_ms, 4)}
+
+    out = {
+        "metric": METRIC,
+        "value": round(NS / (ms_step * 1e-3), 1),
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": describe(cfg), "tables": T, "dim": E, "batch": B,
+                   "pooling": cfg.pooling, "num_indices": NS, "unique_rows": round(U_avg),
+                   "lr": cfg.lr, "batches_rotated": args.batches,
+                   "streams": 2 if args.overlap_prepare else 1},
+        "gbps_alg": round(gbps, 1),
+        "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+        "bytes_alg_per_step": int(step_b),
+        "fwd_ms": round(fwd_ms, 4),
+        "bwd_prepare_ms": round(prep_ms, 4),
+        "bwd_apply_ms": round(apply_ms, 4),
+        "wall_s_timed": round(wall, 3),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        b0 = batches[0]
+        out["cpu_baseline"] = cpu_baseline(cfg, b0["I_host"], b0["G_host"], args.cpu_sample_bags)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -11,6 +11,8 @@ from .generators import (
     splitmix64_np,
     table_values_np,
     table_values_torch,
+    table_rows_torch,
+    fill_table_torch,
     fill_tables_torch,
     make_batch,
     make_grads,
@@ -22,7 +24,7 @@ from .generators import (
 
 __all__ = [
     "BASE_SEED", "Config", "get_config", "CONFIG_NAMES", "scaled",
-    "splitmix64_np", "table_values_np", "table_values_torch",
-    "fill_tables_torch", "make_batch", "make_grads", "random_bags",
+    "splitmix64_np", "table_values_np", "table_values_torch", "table_rows_torch",
+    "fill_table_torch", "fill_tables_torch", "make_batch", "make_grads", "random_bags",
     "zipf_cdf", "row_bijection", "mlperf_rows",
 ]

@@ -97,15 +97,36 @@ def table_values_torch(seed: int, t: int, row_start: int, nrows: int, dim: int,
     return v * float(np.float32(scale))
 
 
+def table_rows_torch(seed: int, t: int, rows, dim: int, scale: float):
+    """Same values as :func:`table_values_np` for arbitrary rows (torch, any device)."""
+    import torch
+    r = torch.as_tensor(rows, dtype=torch.int64)
+    e = torch.arange(dim, dtype=torch.int64, device=r.device)
+    i = ((t << 41) | (r[:, None] << 10)) | e[None, :]
+    z = (i + 1) * _signed(GAMMA) + _signed(table_seed(seed))
+    del i
+    h = _mix_torch(z)
+    del z
+    k = (h >> 40) & ((1 << 24) - 1)
+    del h
+    v = (2 * k + 1 - (1 << 24)).to(torch.float32) * (2.0 ** -24)
+    return v * float(np.float32(scale))
+
+
+def fill_table_torch(cfg, t: int, w, chunk_elems: int = 1 << 26):
+    """Fill a preallocated [M_t, E] FP32 tensor with table t's values (any device)."""
+    m, e = w.shape
+    step = max(1, chunk_elems // e)
+    for r0 in range(0, m, step):
+        n = min(step, m - r0)
+        w[r0:r0 + n].copy_(table_values_torch(cfg.seed, t, r0, n, e, cfg.value_scale[t],
+                                              device=w.device))
+
+
 def fill_tables_torch(cfg, tables, chunk_elems: int = 1 << 26):
     """Fill preallocated [M_t, E] FP32 tensors in place (any device)."""
     for t, w in enumerate(tables):
-        m, e = w.shape
-        step = max(1, chunk_elems // e)
-        for r0 in range(0, m, step):
-            n = min(step, m - r0)
-            w[r0:r0 + n].copy_(table_values_torch(cfg.seed, t, r0, n, e,
-                                                  cfg.value_scale[t], device=w.device))
+        fill_table_torch(cfg, t, w, chunk_elems)
 
 
 # --------------------------------------------------------------------------

@@ -115,6 +115,38 @@ int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* 
                         const embbag_tables_t* tables, void* workspace, size_t workspace_bytes,
                         int32_t* d_status, hipStream_t stream);
 
+/* The fused backward in two phases, for callers that overlap its integer
+ * work with other parts of a training step.  embbag_backward_sgd(...) is
+ * exactly embbag_backward_prepare(...) followed by embbag_backward_apply_sgd(...).
+ *
+ * Phase 1 (Algorithms 2-4's index work): builds the row key of every look-up,
+ * validates offsets and indices, and stably sorts the look-ups by key into
+ * `workspace`.  It reads no gradient, so it may be enqueued as soon as the
+ * batch's indices and offsets exist.  `rows` is a HOST array of num_tables
+ * row counts; `dim` sizes the workspace (embbag_backward_workspace_bytes).
+ * `d_status` (nullable) receives data errors as in the header comment. */
+int embbag_backward_prepare(int32_t num_tables, const int64_t* rows, int32_t dim, int32_t batch,
+                            const int32_t* indices, const int32_t* offsets, int64_t num_indices,
+                            void* workspace, size_t workspace_bytes, int32_t* d_status,
+                            hipStream_t stream);
+
+/* Phase 2: gathers grad_pooled rows per sorted look-up, sums each row's
+ * gradient in FP64 and applies W -= lr * G once per touched row.  The
+ * workspace must hold a phase-1 result for the same batch, num_indices and
+ * table row counts, ordered before this call (same stream, or an event).  If
+ * phase 1 found a data error, or the workspace does not carry a phase-1
+ * result for these sizes, no table row is written.  The same phase-1 result
+ * may be applied more than once (e.g. to several gradients). */
+int embbag_backward_apply_sgd(const float* grad_pooled, int32_t batch, int64_t num_indices,
+                              float lr, const embbag_tables_t* tables, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/* Phase 2 for split tables (Section VII update, as embbag_backward_sgd_split_bf16). */
+int embbag_backward_apply_sgd_split_bf16(const float* grad_pooled, int32_t batch,
+                                         int64_t num_indices, float lr,
+                                         const embbag_split_tables_t* tables, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream);
+
 /* Forward of Section VII: Algorithm 1 reading only the BF16 high halves
  * (each value is hi << 16 as FP32); the low halves are not read. */
 int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch,

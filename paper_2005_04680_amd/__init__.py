@@ -63,6 +63,9 @@ def lib():
         L.embbag_backward_workspace_bytes.restype = sz
         L.embbag_backward_sgd.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz, p, p]
         L.embbag_backward_sgd_split_bf16.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz, p, p]
+        L.embbag_backward_prepare.argtypes = [i32, p, i32, i32, p, p, i64, p, sz, p, p]
+        L.embbag_backward_apply_sgd.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
+        L.embbag_backward_apply_sgd_split_bf16.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
         L.embbag_split_fp32.argtypes = [p, p, p, i64, p]
         L.embbag_combine_fp32.argtypes = [p, p, p, i64, p]
         L.embbag_dedup_workspace_bytes.argtypes = [i32, i32, i64]
@@ -70,8 +73,10 @@ def lib():
         L.embbag_dedup.argtypes = [i32, p, i32, p, p, i64, p, p, p, p, p, p, sz, p, p]
         L.embbag_status_read.argtypes = [p, p]
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
-                  "embbag_backward_sgd_split_bf16", "embbag_split_fp32", "embbag_combine_fp32",
-                  "embbag_dedup", "embbag_status_read"):
+                  "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
+                  "embbag_backward_apply_sgd", "embbag_backward_apply_sgd_split_bf16",
+                  "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
+                  "embbag_status_read"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -193,6 +198,39 @@ def embbag_backward_sgd_split_bf16(grad_pooled, batch, indices, offsets, lr, hi,
         int(indices.numel()), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
         int(workspace.numel() * workspace.element_size()),
         _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_prepare(rows, dim, batch, indices, offsets, workspace, d_status=None,
+                            stream=None) -> int:
+    """Phase 1 of the backward: keys, validation and the sort, into ``workspace``."""
+    T = len(rows)
+    r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
+    return lib().embbag_backward_prepare(T, C.cast(r, C.c_void_p), int(dim), int(batch),
+                                         _ptr(indices, _dt(*_I32), "indices"),
+                                         _ptr(offsets, _dt(*_I32), "offsets"),
+                                         int(indices.numel()), _ptr(workspace, None, "workspace"),
+                                         int(workspace.numel() * workspace.element_size()),
+                                         _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_apply_sgd(grad_pooled, batch, num_indices, lr, weights, workspace,
+                              stream=None) -> int:
+    """Phase 2 of the backward: segment sums and the SGD apply on FP32 tables."""
+    s, keep = _tables_struct(weights)
+    return lib().embbag_backward_apply_sgd(_ptr(grad_pooled, _dt("float32"), "grad_pooled"),
+                                           int(batch), int(num_indices), float(lr), C.byref(s),
+                                           _ptr(workspace, None, "workspace"),
+                                           int(workspace.numel() * workspace.element_size()),
+                                           _stream(stream))
+
+
+def embbag_backward_apply_sgd_split_bf16(grad_pooled, batch, num_indices, lr, hi, lo, workspace,
+                                         stream=None) -> int:
+    s, keep = _tables_struct(hi, split_lo=lo)
+    return lib().embbag_backward_apply_sgd_split_bf16(
+        _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch), int(num_indices), float(lr),
+        C.byref(s), _ptr(workspace, None, "workspace"),
+        int(workspace.numel() * workspace.element_size()), _stream(stream))
 
 
 def embbag_split_fp32(w, hi, lo, stream=None) -> int:

@@ -64,24 +64,54 @@ int forward_common(const TableDesc& d, bool split, int32_t B, const int32_t* I, 
   return hip_status(launch_forward(d, split, B, I, O, NS, Y, d_status, st));
 }
 
+int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O, int64_t NS,
+                   void* ws, size_t ws_bytes, int32_t* d_status, hipStream_t st) {
+  int rc = check_bags(d.num_tables, B, I, O, NS);
+  if (rc) return rc;
+  const uint32_t total = d.rowbase[d.num_tables];
+  const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
+  if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
+  return hip_status(launch_sort(d, B, I, O, NS, L, static_cast<char*>(ws), d_status,
+                                phase_token(d.num_tables, B, NS, total), st));
+}
+
+int apply_common(const TableDesc& d, bool split, const float* dY, int32_t B, int64_t NS, float lr,
+                 void* ws, size_t ws_bytes, hipStream_t st) {
+  if (B < 0 || NS < 0 || NS > kInt32Max || int64_t(d.num_tables) * B + 1 > kInt32Max)
+    return EMBBAG_ERR_INVALID_ARG;
+  if (int64_t(d.num_tables) * B == 0 && NS > 0) return EMBBAG_ERR_OFFSETS;
+  if (NS > 0 && (dY == nullptr || !aligned(dY, 16))) return EMBBAG_ERR_INVALID_ARG;
+  const uint32_t total = d.rowbase[d.num_tables];
+  const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
+  if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
+  return hip_status(launch_segment_sgd(d, split, B, dY, lr, L, static_cast<char*>(ws),
+                                       phase_token(d.num_tables, B, NS, total), st));
+}
+
 int backward_common(const TableDesc& d, bool split, const float* dY, int32_t B, const int32_t* I,
                     const int32_t* O, int64_t NS, float lr, void* ws, size_t ws_bytes,
                     int32_t* d_status, hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
   if (NS > 0 && (dY == nullptr || !aligned(dY, 16))) return EMBBAG_ERR_INVALID_ARG;
-  const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, d.rowbase[d.num_tables], false);
-  if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
-  char* w = static_cast<char*>(ws);
-  uint64_t* sorted = nullptr;
-  hipError_t e = launch_sort(d, B, I, O, NS, L, w, d_status, st, &sorted);
-  if (e != hipSuccess) return EMBBAG_ERR_HIP;
-  return hip_status(launch_segment_sgd(d, split, B, dY, lr, sorted, L, w, st));
+  rc = prepare_common(d, B, I, O, NS, ws, ws_bytes, d_status, st);
+  if (rc) return rc;
+  return apply_common(d, split, dY, B, NS, lr, ws, ws_bytes, st);
 }
 
 }  // namespace
 
 namespace embbag {
+
+uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows) {
+  uint64_t h = 0x243F6A8885A308D3ull;
+  for (uint64_t v : {uint64_t(uint32_t(T)), uint64_t(uint32_t(B)), uint64_t(NS), uint64_t(total_rows)}) {
+    h ^= v + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
+    h *= 0xBF58476D1CE4E5B9ull;
+  }
+  const uint32_t t = uint32_t(h ^ (h >> 32));
+  return t == 0 ? 1u : t;
+}
 
 BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
                           bool for_dedup) {
@@ -196,6 +226,43 @@ int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
                          workspace, workspace_bytes, d_status, stream);
 }
 
+int embbag_backward_prepare(int32_t num_tables, const int64_t* rows, int32_t dim, int32_t batch,
+                            const int32_t* indices, const int32_t* offsets, int64_t num_indices,
+                            void* workspace, size_t workspace_bytes, int32_t* d_status,
+                            hipStream_t stream) {
+  TableDesc d;
+  int rc = make_desc(num_tables, dim, rows, nullptr, nullptr, 0, &d);
+  if (rc) return rc;
+  return prepare_common(d, batch, indices, offsets, num_indices, workspace, workspace_bytes,
+                        d_status, stream);
+}
+
+int embbag_backward_apply_sgd(const float* grad_pooled, int32_t batch, int64_t num_indices,
+                              float lr, const embbag_tables_t* tables, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  return apply_common(d, false, grad_pooled, batch, num_indices, lr, workspace, workspace_bytes,
+                      stream);
+}
+
+int embbag_backward_apply_sgd_split_bf16(const float* grad_pooled, int32_t batch,
+                                         int64_t num_indices, float lr,
+                                         const embbag_split_tables_t* tables, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream) {
+  if (tables == nullptr || tables->lo == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->hi),
+                     reinterpret_cast<void* const*>(tables->lo), 8, &d);
+  if (rc) return rc;
+  return apply_common(d, true, grad_pooled, batch, num_indices, lr, workspace, workspace_bytes,
+                      stream);
+}
+
 int embbag_split_fp32(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t stream) {
   if (n < 0 || (n > 0 && (w == nullptr || hi == nullptr || lo == nullptr)))
     return EMBBAG_ERR_INVALID_ARG;
@@ -233,12 +300,12 @@ int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const i
   if (workspace == nullptr || !aligned(workspace, kWsAlign) || workspace_bytes < L.total)
     return EMBBAG_ERR_WORKSPACE;
   char* w = static_cast<char*>(workspace);
-  uint64_t* sorted = nullptr;
-  if (launch_sort(d, batch, indices, offsets, num_indices, L, w, d_status, stream, &sorted) !=
-      hipSuccess)
+  if (launch_sort(d, batch, indices, offsets, num_indices, L, w, d_status,
+                  phase_token(num_tables, batch, num_indices, d.rowbase[num_tables]),
+                  stream) != hipSuccess)
     return EMBBAG_ERR_HIP;
-  return hip_status(launch_unique(sorted, L, w, sorted_keys, sorted_bags, unique_keys, seg_off,
-                                  d_num_unique, stream));
+  return hip_status(launch_unique(sorted_buffer(L, w), L, w, sorted_keys, sorted_bags,
+                                  unique_keys, seg_off, d_num_unique, stream));
 }
 
 int embbag_status_read(const int32_t* d_status, hipStream_t stream) {

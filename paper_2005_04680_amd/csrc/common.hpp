@@ -69,6 +69,15 @@ __device__ __forceinline__ int wave_id() {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x % kWave; }
 
+// Table of bag k = t*B + b, without an integer division: the FP32 estimate
+// is off by at most one for any k < 2^31 and T <= 64, and is then corrected.
+__device__ __forceinline__ int table_of_bag(uint32_t k, int B, float inv_b) {
+  int t = int(float(k) * inv_b);
+  t -= int(uint32_t(t) * uint32_t(B) > k);
+  t += int(uint32_t(t + 1) * uint32_t(B) <= k);
+  return t;
+}
+
 __device__ __forceinline__ uint32_t key_of(uint64_t p) { return uint32_t(p >> 32); }
 __device__ __forceinline__ uint32_t bag_of(uint64_t p) { return uint32_t(p); }
 
@@ -86,17 +95,27 @@ struct BwdLayout {
 BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
                           bool for_dedup);
 
+// Stamp the sort phase leaves in the workspace for the apply phase: a hash of
+// the sizes the sorted look-ups belong to (never 0).
+uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows);
+
+// The buffer that holds the sorted look-ups after the sort phase.
+inline uint64_t* sorted_buffer(const BwdLayout& L, char* ws) {
+  const int passes = L.ns > 0 ? L.passes : 0;
+  return reinterpret_cast<uint64_t*>(ws + (passes % 2 == 0 ? L.off_a : L.off_b));
+}
+
 hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
                           const int32_t* O, int64_t NS, float* Y, int32_t* status,
                           hipStream_t st);
 
-// Builds keys, validates, sorts; returns the buffer holding the sorted pairs.
+// Builds keys, validates, sorts into sorted_buffer(L, ws); stamps `token`.
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       hipStream_t st, uint64_t** sorted);
+                       uint32_t token, hipStream_t st);
 
 hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
-                              float lr, const uint64_t* sorted, const BwdLayout& L, char* ws,
+                              float lr, const BwdLayout& L, char* ws, uint32_t token,
                               hipStream_t st);
 
 hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,

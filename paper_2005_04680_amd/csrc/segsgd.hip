@@ -3,11 +3,12 @@
 //
 // Input: the look-ups sorted by row key (ties in look-up order), as
 // (key << 32 | bag) words.  The sorted list is cut into fixed chunks of C
-// look-ups, one per row group of LPR lanes.  A row group walks its chunk,
-// gathers dY[bag] for each look-up (U row loads in flight per lane) and adds
-// it to an FP64 accumulator; when the key changes, the finished segment is
+// look-ups, and the E columns into Q slices; one row group of LPR lanes
+// takes one (chunk, slice).  It walks its chunk, gathers the slice of
+// dY[bag] for each look-up (U row loads in flight per lane) and adds it to an
+// FP64 accumulator; when the key changes, the finished segment is
 //   * applied, W[row] <- W[row] - lr * G, if it began and ended inside the
-//     chunk (the W row was prefetched when the segment began), or
+//     chunk (the W row slice was requested with the look-up that began it), or
 //   * parked as a partial sum in the carry buffer: slot 2c for the chunk's
 //     first segment, slot 2c+1 for its last one.
 // A second kernel gives every segment that crosses chunk boundaries to the
@@ -15,6 +16,11 @@
 // of the following chunks, in chunk order, and applies the row once.  Every
 // touched row is therefore read and written exactly once, with a sum order
 // that does not depend on scheduling (the result is bit-reproducible).
+//
+// Locality: each XCD owns one contiguous eighth of the chunks and walks it
+// slice after slice, so the dY rows it gathers at any time are one slice of
+// the bags of one or two tables, which fit its 4 MB L2; the W rows, touched
+// once, are read and written with non-temporal hints so they do not evict it.
 #include "common.hpp"
 
 namespace embbag {
@@ -26,7 +32,8 @@ struct Fp32Rows {
     f4 w;
   };
   static __device__ __forceinline__ Pre load(const TableDesc& d, int t, uint32_t r, int E, int c4) {
-    return {*reinterpret_cast<const f4*>(static_cast<const float*>(d.w[t]) + size_t(r) * E + c4 * 4)};
+    return {__builtin_nontemporal_load(
+        reinterpret_cast<const f4*>(static_cast<const float*>(d.w[t]) + size_t(r) * E + c4 * 4))};
   }
   static __device__ __forceinline__ void store(const TableDesc& d, int t, uint32_t r, int E, int c4,
                                                const Pre& p, const d4& g, double lr) {
@@ -35,7 +42,8 @@ struct Fp32Rows {
     o.y = float(double(p.w.y) - lr * g.y);
     o.z = float(double(p.w.z) - lr * g.z);
     o.w = float(double(p.w.w) - lr * g.w);
-    *reinterpret_cast<f4*>(static_cast<float*>(d.w[t]) + size_t(r) * E + c4 * 4) = o;
+    __builtin_nontemporal_store(
+        o, reinterpret_cast<f4*>(static_cast<float*>(d.w[t]) + size_t(r) * E + c4 * 4));
   }
 };
 
@@ -47,8 +55,8 @@ struct SplitRows {
   };
   static __device__ __forceinline__ Pre load(const TableDesc& d, int t, uint32_t r, int E, int c4) {
     const size_t off = size_t(r) * E + c4 * 4;
-    return {*reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.w[t]) + off),
-            *reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.lo[t]) + off)};
+    return {__builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.w[t]) + off)),
+            __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.lo[t]) + off))};
   }
   static __device__ __forceinline__ float upd(uint32_t hi16, uint32_t lo16, double g, double lr) {
     const float w = __uint_as_float((hi16 << 16) | lo16);
@@ -66,8 +74,8 @@ struct SplitRows {
     lo.x = (w0 & 0xFFFFu) | (w1 << 16);
     lo.y = (w2 & 0xFFFFu) | (w3 << 16);
     const size_t off = size_t(r) * E + c4 * 4;
-    *reinterpret_cast<u2*>(static_cast<uint16_t*>(d.w[t]) + off) = hi;
-    *reinterpret_cast<u2*>(static_cast<uint16_t*>(d.lo[t]) + off) = lo;
+    __builtin_nontemporal_store(hi, reinterpret_cast<u2*>(static_cast<uint16_t*>(d.w[t]) + off));
+    __builtin_nontemporal_store(lo, reinterpret_cast<u2*>(static_cast<uint16_t*>(d.lo[t]) + off));
   }
 };
 
@@ -76,30 +84,41 @@ __device__ __forceinline__ d4 widen(const f4& v) {
 }
 
 template <int CPL>
-__device__ __forceinline__ void store_carry(double* carry, int64_t slot, int E, int rl, int lpr,
-                                            const d4* acc) {
+__device__ __forceinline__ void store_carry(double* carry, int64_t slot, int E, int cbase,
+                                            int e4s, int rl, int lpr, const d4* acc) {
   double* c = carry + slot * E;
 #pragma unroll
   for (int j = 0; j < CPL; ++j) {
     const int c4 = rl + j * lpr;
-    if (c4 < E / 4) *reinterpret_cast<d4*>(c + c4 * 4) = acc[j];
+    if (c4 < e4s) *reinterpret_cast<d4*>(c + (cbase + c4) * 4) = acc[j];
   }
 }
 
 template <int LPR, int CPL, class Rows>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
-    const float* __restrict__ dY, int32_t B, float lr, double* __restrict__ carry,
-    const int32_t* __restrict__ flags) {
-  if (flags[0] != 0) return;  // data error: no table writes
+    int32_t Q, int32_t cpp, const float* __restrict__ dY, int32_t B, float inv_b, float lr,
+    double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token) {
+  // A data error, or no sort result for these sizes: no table writes.
+  if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
-  constexpr int U = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
-  const int E = d.dim, E4 = E / 4;
+  // look-ups in flight per row group: fewer when a wave holds several row
+  // groups (their (key, bag) words no longer share scalar registers)
+  constexpr int U = CPL == 1 ? (LPR == kWave ? 8 : 4) : (CPL == 2 ? 4 : 2);
+  const int E = d.dim;
+  const int e4s = E / 4 / Q;  // float4 groups per slice
   const int lane = lane_id();
   const int rg = lane / LPR, rl = lane % LPR;
+  // unit = (part * Q + slice) * cpp + i: part p (one per XCD) owns chunks
+  // [p*cpp, (p+1)*cpp), visited slice by slice.
   const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
-  const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
+  const int unit = (blk * kWavesPerBlock + wave_id()) * R + rg;
+  const int part = unit / (Q * cpp);
+  const int rem = unit - part * Q * cpp;
+  const int q = rem / cpp;
+  const int chunk = part * cpp + (rem - q * cpp);
   if (chunk >= nchunks) return;
+  const int cbase = q * e4s;
   const int lo = chunk * C, hi = min(lo + C, NS);
   const double lrd = double(lr);
 
@@ -107,76 +126,107 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   const uint32_t knext = hi < NS ? key_of(sorted[hi]) : kNoKey;
   const uint64_t p0 = sorted[lo];
   uint32_t cur = key_of(p0);
-  int ct = int(bag_of(p0) / uint32_t(B));
+  int ct = table_of_bag(bag_of(p0), B, inv_b);
   const bool first_open = kprev == cur;  // first segment began in an earlier chunk
   bool is_first = true;
 
   d4 acc[CPL];
+  f4 glast[CPL];
   typename Rows::Pre pre[CPL];
 #pragma unroll
   for (int j = 0; j < CPL; ++j) {
     acc[j] = d4{0.0, 0.0, 0.0, 0.0};
+    glast[j] = f4{0.f, 0.f, 0.f, 0.f};
     const int c4 = rl + j * LPR;
-    if (!first_open && c4 < E4) pre[j] = Rows::load(d, ct, cur - d.rowbase[ct], E, c4);
+    if (!first_open && c4 < e4s) pre[j] = Rows::load(d, ct, cur - d.rowbase[ct], E, cbase + c4);
   }
 
+  auto apply = [&](uint32_t key, int t) {
+    const uint32_t r = key - d.rowbase[t];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c4 = rl + j * LPR;
+      if (c4 < e4s) Rows::store(d, t, r, E, cbase + c4, pre[j], acc[j], lrd);
+    }
+  };
+
+  // Software pipeline: the (key, bag) words of the next U look-ups are loaded
+  // while the current ones are summed; for the current U look-ups, the dY rows
+  // (skipped when a look-up repeats the previous (key, bag) pair: its row is
+  // still in registers) and the W rows of the segments that start among them
+  // are all requested before the first of them is used.
+  uint64_t pn[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) pn[u] = lo + u < hi ? sorted[lo + u] : 0ull;
+  uint64_t plast = p0;  // look-up before the current group (none before lo: p0 itself)
   for (int s = lo; s < hi; s += U) {
     uint64_t p[U];
+    bool dup[U], nseg[U];
     f4 g[U][CPL];
-#pragma unroll
-    for (int u = 0; u < U; ++u) p[u] = s + u < hi ? sorted[s + u] : 0ull;
+    typename Rows::Pre wp[U][CPL];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float* gy = dY + size_t(bag_of(p[u])) * E;
-#pragma unroll
-      for (int j = 0; j < CPL; ++j) {
-        const int c4 = rl + j * LPR;
-        g[u][j] = (s + u < hi && c4 < E4) ? *reinterpret_cast<const f4*>(gy + c4 * 4)
-                                          : f4{0.f, 0.f, 0.f, 0.f};
-      }
+      p[u] = pn[u];
+      const uint64_t pq = u == 0 ? plast : p[u - 1];
+      const bool valid = s + u < hi;
+      dup[u] = valid && p[u] == pq && !(s == lo && u == 0);
+      nseg[u] = valid && key_of(p[u]) != key_of(pq);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (s + u >= hi) break;
-      const uint32_t key = key_of(p[u]);
-      if (key != cur) {
-        if (is_first && first_open) {
-          store_carry<CPL>(carry, 2 * int64_t(chunk), E, rl, LPR, acc);
-        } else {
-          const uint32_t r = cur - d.rowbase[ct];
+      const float* gy = dY + size_t(bag_of(p[u])) * E + cbase * 4;
+      const bool ld = s + u < hi && !dup[u];
 #pragma unroll
-          for (int j = 0; j < CPL; ++j) {
-            const int c4 = rl + j * LPR;
-            if (c4 < E4) Rows::store(d, ct, r, E, c4, pre[j], acc[j], lrd);
-          }
+      for (int j = 0; j < CPL; ++j) {
+        const int c4 = rl + j * LPR;
+        g[u][j] = (ld && c4 < e4s) ? *reinterpret_cast<const f4*>(gy + c4 * 4)
+                                   : f4{0.f, 0.f, 0.f, 0.f};
+      }
+      if (nseg[u]) {
+        const int tu = table_of_bag(bag_of(p[u]), B, inv_b);
+        const uint32_t ru = key_of(p[u]) - d.rowbase[tu];
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+          const int c4 = rl + j * LPR;
+          if (c4 < e4s) wp[u][j] = Rows::load(d, tu, ru, E, cbase + c4);
         }
-        cur = key;
-        ct = int(bag_of(p[u]) / uint32_t(B));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) pn[u] = s + U + u < hi ? sorted[s + U + u] : 0ull;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s + u >= hi) break;
+      if (nseg[u]) {
+        if (is_first && first_open)
+          store_carry<CPL>(carry, 2 * int64_t(chunk), E, cbase, e4s, rl, LPR, acc);
+        else
+          apply(cur, ct);
+        cur = key_of(p[u]);
+        ct = table_of_bag(bag_of(p[u]), B, inv_b);
         is_first = false;
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
           acc[j] = d4{0.0, 0.0, 0.0, 0.0};
-          const int c4 = rl + j * LPR;
-          if (c4 < E4) pre[j] = Rows::load(d, ct, cur - d.rowbase[ct], E, c4);
+          pre[j] = wp[u][j];
         }
       }
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) acc[j] += widen(g[u][j]);
+      for (int j = 0; j < CPL; ++j) {
+        if (!dup[u]) glast[j] = g[u][j];
+        acc[j] += widen(glast[j]);
+      }
     }
+    plast = p[U - 1];
   }
 
   const bool last_open = knext == cur;  // last segment continues in the next chunk
   if (is_first && (first_open || last_open)) {
-    store_carry<CPL>(carry, 2 * int64_t(chunk), E, rl, LPR, acc);
+    store_carry<CPL>(carry, 2 * int64_t(chunk), E, cbase, e4s, rl, LPR, acc);
   } else if (!is_first && last_open) {
-    store_carry<CPL>(carry, 2 * int64_t(chunk) + 1, E, rl, LPR, acc);
+    store_carry<CPL>(carry, 2 * int64_t(chunk) + 1, E, cbase, e4s, rl, LPR, acc);
   } else {
-    const uint32_t r = cur - d.rowbase[ct];
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-      const int c4 = rl + j * LPR;
-      if (c4 < E4) Rows::store(d, ct, r, E, c4, pre[j], acc[j], lrd);
-    }
+    apply(cur, ct);
   }
 }
 
@@ -185,8 +235,9 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
 template <int LPR, int CPL, class Rows>
 __global__ __launch_bounds__(kBlock) void segment_fixup(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
-    int32_t B, float lr, const double* __restrict__ carry, const int32_t* __restrict__ flags) {
-  if (flags[0] != 0) return;
+    int32_t B, float inv_b, float lr, const double* __restrict__ carry,
+    const int32_t* __restrict__ flags, uint32_t token) {
+  if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
   constexpr int UF = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
   const int E = d.dim, E4 = E / 4;
@@ -200,7 +251,7 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   if (key_of(sorted[hi]) != kl) return;             // last segment ends here
   const uint32_t kf = key_of(sorted[lo]);
   if (kf == kl && lo > 0 && key_of(sorted[lo - 1]) == kl) return;  // began earlier
-  const int ct = int(bag_of(sorted[hi - 1]) / uint32_t(B));
+  const int ct = table_of_bag(bag_of(sorted[hi - 1]), B, inv_b);
   const uint32_t r = kl - d.rowbase[ct];
   const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
 
@@ -251,21 +302,14 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   }
 }
 
-template <class Rows, int LPR, int CPL>
-void launch_pair(int blocks_seg, int blocks_fix, hipStream_t st, const TableDesc& d,
-                 const uint64_t* sorted, int32_t NS, int32_t C, int32_t nchunks, const float* dY,
-                 int32_t B, float lr, double* carry, const int32_t* flags) {
-  hipLaunchKernelGGL((segment_sgd<LPR, CPL, Rows>), dim3(blocks_seg), dim3(kBlock), 0, st, d,
-                     sorted, NS, C, nchunks, dY, B, lr, carry, flags);
-  hipLaunchKernelGGL((segment_fixup<LPR, CPL, Rows>), dim3(blocks_fix), dim3(kBlock), 0, st, d,
-                     sorted, NS, C, nchunks, B, lr, carry, flags);
-}
-
 template <class Rows>
-bool dispatch(RowGeom g, int bs, int bf, hipStream_t st, const TableDesc& d,
-              const uint64_t* sorted, int32_t NS, int32_t C, int32_t nchunks, const float* dY,
-              int32_t B, float lr, double* carry, const int32_t* flags) {
-#define EMB_SEG(L, CC) launch_pair<Rows, L, CC>(bs, bf, st, d, sorted, NS, C, nchunks, dY, B, lr, carry, flags)
+bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
+                int32_t NS, int32_t C, int32_t nchunks, int32_t Q, int32_t cpp, const float* dY,
+                int32_t B, float inv_b, float lr, double* carry, const int32_t* flags,
+                uint32_t token) {
+#define EMB_SEG(L, CC)                                                                        \
+  hipLaunchKernelGGL((segment_sgd<L, CC, Rows>), dim3(blocks), dim3(kBlock), 0, st, d, sorted, \
+                     NS, C, nchunks, Q, cpp, dY, B, inv_b, lr, carry, flags, token)
   switch (g.lpr) {
     case 1: EMB_SEG(1, 1); return true;
     case 2: EMB_SEG(2, 1); return true;
@@ -285,23 +329,73 @@ bool dispatch(RowGeom g, int bs, int bf, hipStream_t st, const TableDesc& d,
   return false;
 }
 
+template <class Rows>
+bool launch_fix(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
+                int32_t NS, int32_t C, int32_t nchunks, int32_t B, float inv_b, float lr,
+                const double* carry, const int32_t* flags, uint32_t token) {
+#define EMB_FIX(L, CC)                                                                          \
+  hipLaunchKernelGGL((segment_fixup<L, CC, Rows>), dim3(blocks), dim3(kBlock), 0, st, d, sorted, \
+                     NS, C, nchunks, B, inv_b, lr, carry, flags, token)
+  switch (g.lpr) {
+    case 1: EMB_FIX(1, 1); return true;
+    case 2: EMB_FIX(2, 1); return true;
+    case 4: EMB_FIX(4, 1); return true;
+    case 8: EMB_FIX(8, 1); return true;
+    case 16: EMB_FIX(16, 1); return true;
+    case 32: EMB_FIX(32, 1); return true;
+    case 64:
+      switch (g.cpl) {
+        case 1: EMB_FIX(64, 1); return true;
+        case 2: EMB_FIX(64, 2); return true;
+        case 3: EMB_FIX(64, 3); return true;
+        case 4: EMB_FIX(64, 4); return true;
+      }
+  }
+#undef EMB_FIX
+  return false;
+}
+
 }  // namespace
 
+int apply_slices(int dim) {
+  // Slices of 64 columns (256 B of a row) for wide rows: a slice of the dY
+  // rows of one table (B x 256 B, 2 MB at B = 8192) fits one XCD's L2.
+  int q = 1;  // measured on MI355X: slicing trades fabric bytes for issue-bound time
+  (void)dim;
+  if (q < 1) q = 1;
+  if (q > 4) q = 4;
+  while (q > 1 && dim % (4 * q) != 0) --q;
+  return q;
+}
+
 hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
-                              float lr, const uint64_t* sorted, const BwdLayout& L, char* ws,
+                              float lr, const BwdLayout& L, char* ws, uint32_t token,
                               hipStream_t st) {
   if (L.ns == 0) return hipSuccess;
+  const uint64_t* sorted = sorted_buffer(L, ws);
   double* carry = reinterpret_cast<double*>(ws + L.off_carry);
   const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
-  const RowGeom g = row_geom(d.dim);
-  const int per_block = kWavesPerBlock * (kWave / g.lpr);
-  const int blocks = int((L.nchunks + per_block - 1) / per_block);
-  const bool ok = split ? dispatch<SplitRows>(g, blocks, blocks, st, d, sorted, int32_t(L.ns),
-                                              int32_t(L.chunk), int32_t(L.nchunks), dY, B, lr,
-                                              carry, flags)
-                        : dispatch<Fp32Rows>(g, blocks, blocks, st, d, sorted, int32_t(L.ns),
-                                             int32_t(L.chunk), int32_t(L.nchunks), dY, B, lr,
-                                             carry, flags);
+  const float inv_b = 1.0f / float(B);
+  const int Q = apply_slices(d.dim);
+  const RowGeom gs = row_geom(d.dim / Q);
+  const int per_block = kWavesPerBlock * (kWave / gs.lpr);
+  // chunks per part (one part per XCD), a whole number of blocks
+  int64_t cpp = (L.nchunks + kNumXcd - 1) / kNumXcd;
+  cpp = (cpp + per_block - 1) / per_block * per_block;
+  const int blocks_seg = int(kNumXcd * Q * cpp / per_block);
+  const RowGeom gf = row_geom(d.dim);
+  const int per_block_f = kWavesPerBlock * (kWave / gf.lpr);
+  const int blocks_fix = int((L.nchunks + per_block_f - 1) / per_block_f);
+  const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
+  bool ok = split ? launch_seg<SplitRows>(gs, blocks_seg, st, d, sorted, NS, C, nch, Q,
+                                          int32_t(cpp), dY, B, inv_b, lr, carry, flags, token)
+                  : launch_seg<Fp32Rows>(gs, blocks_seg, st, d, sorted, NS, C, nch, Q,
+                                         int32_t(cpp), dY, B, inv_b, lr, carry, flags, token);
+  if (ok)
+    ok = split ? launch_fix<SplitRows>(gf, blocks_fix, st, d, sorted, NS, C, nch, B, inv_b, lr,
+                                       carry, flags, token)
+               : launch_fix<Fp32Rows>(gf, blocks_fix, st, d, sorted, NS, C, nch, B, inv_b, lr,
+                                      carry, flags, token);
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -52,7 +52,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
 // a slice of the bags; one status word per block.
 __global__ __launch_bounds__(kBlock) void build_keys(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
-    int32_t B, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
+    int32_t B, float inv_b, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
     uint32_t* __restrict__ hist, int32_t* __restrict__ parts) {
   __shared__ uint32_t lbag[kTile];
   __shared__ uint32_t lhist[kRadix];
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kBlock) void build_keys(
       const int s = s_lo + i * kBlock + tid;
       if (s < s_hi) {
         const uint32_t k = min(lbag[s - s_lo], uint32_t(TB - 1));
-        const uint32_t t = k / uint32_t(B);
+        const int t = table_of_bag(k, B, inv_b);
         int32_t r = I[s];
         if (uint32_t(r) >= d.rows[t]) {
           err = min(err, EMBBAG_ERR_INDEX_RANGE);
@@ -144,7 +144,8 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
                                                      uint32_t* __restrict__ totals,
                                                      const int32_t* __restrict__ parts,
                                                      int32_t nparts, int32_t* __restrict__ flags,
-                                                     int32_t* __restrict__ d_status) {
+                                                     int32_t* __restrict__ d_status,
+                                                     uint32_t token) {
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   __shared__ int32_t lerr;
   const int tid = threadIdx.x;
@@ -157,6 +158,7 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
     __syncthreads();
     if (tid == 0) {
       flags[0] = lerr;
+      flags[1] = int32_t(token);
       if (lerr != 0 && d_status != nullptr) atomicMin(d_status, lerr);
     }
     return;
@@ -332,7 +334,7 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
 
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       hipStream_t st, uint64_t** sorted) {
+                       uint32_t token, hipStream_t st) {
   const int32_t TB = d.num_tables * B;
   uint64_t* a = reinterpret_cast<uint64_t*>(ws + L.off_a);
   uint64_t* b = reinterpret_cast<uint64_t*>(ws + L.off_b);
@@ -343,14 +345,14 @@ hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const in
   const int nkb = int(L.nkeyblocks);
   const int vb = (TB + 1 + nkb - 1) / nkb;
   const int ntiles = int(L.ntiles);
-  hipLaunchKernelGGL(build_keys, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B, TB,
-                     ntiles, vb, a, hist, parts);
+  const float inv_b = B > 0 ? 1.0f / float(B) : 0.0f;
+  hipLaunchKernelGGL(build_keys, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B, inv_b,
+                     TB, ntiles, vb, a, hist, parts);
   // Status verdict (block 256 of the first scan, or alone when nothing is sorted).
   const int passes = NS > 0 ? L.passes : 0;
   if (passes == 0) {
     hipLaunchKernelGGL(radix_scan, dim3(kRadix + 1), dim3(kBlock), 0, st, hist, 0, totals, parts,
-                       nkb, flags, d_status);
-    *sorted = a;
+                       nkb, flags, d_status, token);
     return hipGetLastError();
   }
   uint64_t* src = a;
@@ -361,14 +363,13 @@ hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const in
       hipLaunchKernelGGL(radix_upsweep, dim3(ntiles), dim3(kBlock), 0, st, src, int32_t(NS),
                          shift, ntiles, hist);
     hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? kRadix + 1 : kRadix), dim3(kBlock), 0, st, hist,
-                       ntiles, totals, parts, nkb, flags, d_status);
+                       ntiles, totals, parts, nkb, flags, d_status, token);
     hipLaunchKernelGGL(radix_downsweep, dim3(ntiles), dim3(kBlock), 0, st, src, dst,
                        int32_t(NS), shift, ntiles, hist, totals);
     uint64_t* tmp = src;
     src = dst;
     dst = tmp;
   }
-  *sorted = src;
   return hipGetLastError();
 }
 

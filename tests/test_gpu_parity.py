@@ -277,3 +277,65 @@ def test_split_helpers_bit_exact():
     back = torch.empty_like(wd)
     assert pk.embbag_combine_fp32(hi, lo, back) == 0
     assert bits_equal(back.cpu().numpy(), w)
+
+
+# ---------------------------------------------------------------------------
+# Two-phase backward (prepare = index work, apply = segment sums + SGD)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("split", [False, True])
+def test_prepare_apply_equals_fused(split):
+    import paper_2005_04680_amd as pk
+    rng = np.random.default_rng(21)
+    rows = (3000, 17, 900)
+    dim = 64
+    W = _tables(rng, rows, dim, 0.05)
+    I, O = random_bags(rng, rows, 300, 25, 0.05, 0.3)
+    G = rng.standard_normal((3, 300, dim)).astype(np.float32)
+    fused = GpuTables(W, split=split)
+    assert fused.backward(G, 300, I, O, 0.1) == 0
+    two = GpuTables(W, split=split)
+    Id, Od, Gd = to_dev(I), to_dev(O), to_dev(G)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(3, 300, I.size, dim), dtype=torch.uint8,
+                     device=DEV)
+    assert pk.embbag_backward_prepare(rows, dim, 300, Id, Od, ws, two.status) == 0
+    if split:
+        rc = pk.embbag_backward_apply_sgd_split_bf16(Gd, 300, I.size, 0.1, two.w, two.lo, ws)
+    else:
+        rc = pk.embbag_backward_apply_sgd(Gd, 300, I.size, 0.1, two.w, ws)
+    assert rc == 0 and two.read_status() == 0
+    for a, b in zip(fused.host(), two.host()):
+        assert bits_equal(a, b)
+
+
+def test_apply_needs_a_prepared_workspace():
+    import paper_2005_04680_amd as pk
+    rng = np.random.default_rng(22)
+    rows = (500, 500)
+    W = _tables(rng, rows, 32, 0.05)
+    I, O = random_bags(rng, rows, 100, 10, 0.0, 0.2)
+    G = rng.standard_normal((2, 100, 32)).astype(np.float32)
+    gt = GpuTables(W)
+    Id, Od, Gd = to_dev(I), to_dev(O), to_dev(G)
+    ws = torch.zeros(pk.embbag_backward_workspace_bytes(2, 100, I.size, 32), dtype=torch.uint8,
+                     device=DEV)
+    # never prepared: nothing is written
+    assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
+    for a, b in zip(gt.host(), W):
+        assert bits_equal(a, b)
+    # prepared once, applied twice: two SGD steps with the same gradient
+    assert pk.embbag_backward_prepare(rows, 32, 100, Id, Od, ws, gt.status) == 0
+    assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
+    assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd(G, 100, I, O, 0.1, Wref) == 0
+    assert oracle.backward_sgd(G, 100, I, O, 0.1, Wref) == 0
+    for t, (a, b) in enumerate(zip(gt.host(), Wref)):
+        assert_close(a, b, f"two applies table {t}")
+    # a prepare for other sizes leaves a stamp the apply rejects
+    I2, O2 = random_bags(rng, rows, 100, 10, 0.0, 0.2)
+    assert pk.embbag_backward_prepare(rows, 32, 100, to_dev(I2), to_dev(O2), ws, gt.status) == 0
+    before = gt.host()
+    if I2.size != I.size:
+        assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
+        for a, b in zip(gt.host(), before):
+            assert bits_equal(a, b)
