@@ -31,7 +31,7 @@ __device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, int E, i
   }
 }
 
-template <int LPR, int CPL, bool SPLIT>
+template <int LPR, int CPL, bool SPLIT, bool MULTI>
 __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, int32_t G, int32_t groups_per_table, int32_t items, float* __restrict__ Y,
@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   const int TB = d.num_tables * B;
   const int t = item / groups_per_table;
   const int k0 = t * B + (item - t * groups_per_table) * G;
-  const int k1 = min(k0 + G, (t + 1) * B);
+  const int k1 = MULTI ? min(k0 + G, (t + 1) * B) : k0 + 1;
   const uint32_t M = d.rows[t];
   const void* base = d.w[t];
   int err = 0;
@@ -67,59 +67,98 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   if ((k0 == 0 && s0 != 0) || (k1 == TB && s1 != NS)) err = EMBBAG_ERR_OFFSETS;
   bool bad = s0 < 0 || s1 > NS || s0 > s1;
   int k = k0;
-  int bound = bad ? 0 : O[k0 + 1];
-  bad = bad || bound < s0 || bound > s1;
+  int bound = s1;
+  if constexpr (MULTI) {
+    bound = bad ? 0 : O[k0 + 1];
+    bad = bad || bound < s0 || bound > s1;
+  }
 
   f4 acc[CPL];
 #pragma unroll
   for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
 
+  // Indices arrive in windows of LPR look-ups, one per lane of the row group
+  // (a coalesced load), the next window already in flight; each look-up's
+  // index is then broadcast from its lane, so the row loads of an iteration
+  // do not wait on index loads.  Past the end of the group a slot re-reads
+  // the group's last row, and an index outside its table reads row 0: every
+  // load is valid, and such slots are masked out of the sum.
+  constexpr bool kWin = LPR >= U;
+  int wbase = s0, vcur = 0, vnext = 0;
+  if constexpr (kWin) {
+    if (!bad) {
+      vcur = s0 + rl < s1 ? I[s0 + rl] : 0;
+      vnext = s0 + LPR + rl < s1 ? I[s0 + LPR + rl] : 0;
+    }
+  }
+
   for (int s = s0; s < s1 && !bad; s += U) {
+    if constexpr (kWin) {
+      if (s - wbase >= LPR) {
+        wbase += LPR;
+        vcur = vnext;
+        vnext = wbase + LPR + rl < s1 ? I[wbase + LPR + rl] : 0;
+      }
+    }
     f4 v[U][CPL];
+    bool use[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int ss = s + u;
-      const int idx = ss < s1 ? I[ss] : 0;
-      const bool ok = ss < s1 && uint32_t(idx) < M;
-      if (ss < s1 && !ok) err = min(err, EMBBAG_ERR_INDEX_RANGE);
+      const int ss = min(s + u, s1 - 1);
+      int idx;
+      if constexpr (kWin) {
+        if constexpr (LPR == kWave)
+          idx = __builtin_amdgcn_readlane(vcur, ss - wbase);
+        else
+          idx = __shfl(vcur, rg * LPR + (ss - wbase), kWave);
+      } else {
+        idx = I[ss];
+      }
+      const bool ok = uint32_t(idx) < M;
+      if (!ok) err = min(err, EMBBAG_ERR_INDEX_RANGE);
+      use[u] = ok && s + u < s1;
+      const uint32_t row = ok ? uint32_t(idx) : 0u;
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
-        const int c4 = rl + j * LPR;
-        v[u][j] = (ok && c4 < E4) ? load_row4<SPLIT>(base, uint32_t(idx), E, c4)
-                                  : f4{0.f, 0.f, 0.f, 0.f};
+        const int c4 = min(rl + j * LPR, E4 - 1);
+        v[u][j] = load_row4<SPLIT>(base, row, E, c4);
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int ss = s + u;
-      if (ss >= s1 || bad) break;
-      // Crossing the end of bag k (and of any empty bags after it).  While
-      // ss < s1 = O[k1] and O is non-decreasing up to s1, k + 1 < k1 here.
-      while (ss >= bound) {
-        store_bag(k, acc);
+      if constexpr (MULTI) {
+        const int ss = s + u;
+        if (ss >= s1 || bad) break;
+        // Crossing the end of bag k (and of any empty bags after it).  While
+        // ss < s1 = O[k1] and O is non-decreasing up to s1, k + 1 < k1 here.
+        while (ss >= bound) {
+          store_bag(k, acc);
 #pragma unroll
-        for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-        ++k;
-        const int nb = O[k + 1];
-        if (nb < bound || nb > s1) {
-          bad = true;
-          break;
+          for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+          ++k;
+          const int nb = O[k + 1];
+          if (nb < bound || nb > s1) {
+            bad = true;
+            break;
+          }
+          bound = nb;
         }
-        bound = nb;
+        if (bad) break;
       }
-      if (bad) break;
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) acc[j] += v[u][j];
+      for (int j = 0; j < CPL; ++j) acc[j] = use[u] ? acc[j] + v[u][j] : acc[j];
     }
   }
   if (!bad) {
     store_bag(k, acc);
-    // Remaining bags of the group hold no look-ups: O[k'] == s1 for them all.
-    for (int kk = k + 1; kk < k1; ++kk) {
-      if (O[kk] != s1) bad = true;
+    if constexpr (MULTI) {
+      // Remaining bags of the group hold no look-ups: O[k'] == s1 for them all.
+      for (int kk = k + 1; kk < k1; ++kk) {
+        if (O[kk] != s1) bad = true;
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-      store_bag(kk, acc);
+        for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+        store_bag(kk, acc);
+      }
     }
   }
   if (bad) err = EMBBAG_ERR_OFFSETS;
@@ -137,8 +176,12 @@ template <bool SPLIT, int LPR, int CPL>
 void launch_one(dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I, const int32_t* O,
                 int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items, float* Y,
                 int32_t* status) {
-  hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT>), grid, dim3(kBlock), 0, st, d, I, O, NS,
-                     B, G, gpt, items, Y, status);
+  if (G > 1)
+    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, true>), grid, dim3(kBlock), 0, st, d, I, O,
+                       NS, B, G, gpt, items, Y, status);
+  else
+    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, false>), grid, dim3(kBlock), 0, st, d, I,
+                       O, NS, B, G, gpt, items, Y, status);
 }
 
 template <bool SPLIT>

@@ -3,12 +3,11 @@
 //
 // Input: the look-ups sorted by row key (ties in look-up order), as
 // (key << 32 | bag) words.  The sorted list is cut into fixed chunks of C
-// look-ups, and the E columns into Q slices; one row group of LPR lanes
-// takes one (chunk, slice).  It walks its chunk, gathers the slice of
-// dY[bag] for each look-up (U row loads in flight per lane) and adds it to an
-// FP64 accumulator; when the key changes, the finished segment is
+// look-ups, one per row group of LPR lanes.  A row group walks its chunk,
+// gathers dY[bag] for each look-up (U row loads in flight per lane) and adds
+// it to an FP64 accumulator; when the key changes, the finished segment is
 //   * applied, W[row] <- W[row] - lr * G, if it began and ended inside the
-//     chunk (the W row slice was requested with the look-up that began it), or
+//     chunk (the W row was requested with the look-up that began it), or
 //   * parked as a partial sum in the carry buffer: slot 2c for the chunk's
 //     first segment, slot 2c+1 for its last one.
 // A second kernel gives every segment that crosses chunk boundaries to the
@@ -17,10 +16,9 @@
 // touched row is therefore read and written exactly once, with a sum order
 // that does not depend on scheduling (the result is bit-reproducible).
 //
-// Locality: each XCD owns one contiguous eighth of the chunks and walks it
-// slice after slice, so the dY rows it gathers at any time are one slice of
-// the bags of one or two tables, which fit its 4 MB L2; the W rows, touched
-// once, are read and written with non-temporal hints so they do not evict it.
+// Locality: each XCD owns one contiguous range of chunks, so the dY rows it
+// gathers at any time belong to one or two tables; the W rows, touched once,
+// are read and written with non-temporal hints so they do not evict them.
 #include "common.hpp"
 
 namespace embbag {
@@ -84,20 +82,20 @@ __device__ __forceinline__ d4 widen(const f4& v) {
 }
 
 template <int CPL>
-__device__ __forceinline__ void store_carry(double* carry, int64_t slot, int E, int cbase,
-                                            int e4s, int rl, int lpr, const d4* acc) {
+__device__ __forceinline__ void store_carry(double* carry, int64_t slot, int E, int rl, int lpr,
+                                            const d4* acc) {
   double* c = carry + slot * E;
 #pragma unroll
   for (int j = 0; j < CPL; ++j) {
     const int c4 = rl + j * lpr;
-    if (c4 < e4s) *reinterpret_cast<d4*>(c + (cbase + c4) * 4) = acc[j];
+    if (c4 < E / 4) *reinterpret_cast<d4*>(c + c4 * 4) = acc[j];
   }
 }
 
 template <int LPR, int CPL, class Rows>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
-    int32_t Q, int32_t cpp, const float* __restrict__ dY, int32_t B, float inv_b, float lr,
+    const float* __restrict__ dY, int32_t B, float inv_b, float lr,
     double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token) {
   // A data error, or no sort result for these sizes: no table writes.
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
@@ -106,19 +104,12 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   // groups (their (key, bag) words no longer share scalar registers)
   constexpr int U = CPL == 1 ? (LPR == kWave ? 8 : 4) : (CPL == 2 ? 4 : 2);
   const int E = d.dim;
-  const int e4s = E / 4 / Q;  // float4 groups per slice
+  const int E4 = E / 4;  // float4 groups per row
   const int lane = lane_id();
   const int rg = lane / LPR, rl = lane % LPR;
-  // unit = (part * Q + slice) * cpp + i: part p (one per XCD) owns chunks
-  // [p*cpp, (p+1)*cpp), visited slice by slice.
   const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
-  const int unit = (blk * kWavesPerBlock + wave_id()) * R + rg;
-  const int part = unit / (Q * cpp);
-  const int rem = unit - part * Q * cpp;
-  const int q = rem / cpp;
-  const int chunk = part * cpp + (rem - q * cpp);
+  const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
-  const int cbase = q * e4s;
   const int lo = chunk * C, hi = min(lo + C, NS);
   const double lrd = double(lr);
 
@@ -138,7 +129,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     acc[j] = d4{0.0, 0.0, 0.0, 0.0};
     glast[j] = f4{0.f, 0.f, 0.f, 0.f};
     const int c4 = rl + j * LPR;
-    if (!first_open && c4 < e4s) pre[j] = Rows::load(d, ct, cur - d.rowbase[ct], E, cbase + c4);
+    if (!first_open && c4 < E4) pre[j] = Rows::load(d, ct, cur - d.rowbase[ct], E, c4);
   }
 
   auto apply = [&](uint32_t key, int t) {
@@ -146,7 +137,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
       const int c4 = rl + j * LPR;
-      if (c4 < e4s) Rows::store(d, t, r, E, cbase + c4, pre[j], acc[j], lrd);
+      if (c4 < E4) Rows::store(d, t, r, E, c4, pre[j], acc[j], lrd);
     }
   };
 
@@ -174,12 +165,12 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float* gy = dY + size_t(bag_of(p[u])) * E + cbase * 4;
+      const float* gy = dY + size_t(bag_of(p[u])) * E;
       const bool ld = s + u < hi && !dup[u];
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int c4 = rl + j * LPR;
-        g[u][j] = (ld && c4 < e4s) ? *reinterpret_cast<const f4*>(gy + c4 * 4)
+        g[u][j] = (ld && c4 < E4) ? *reinterpret_cast<const f4*>(gy + c4 * 4)
                                    : f4{0.f, 0.f, 0.f, 0.f};
       }
       if (nseg[u]) {
@@ -188,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
           const int c4 = rl + j * LPR;
-          if (c4 < e4s) wp[u][j] = Rows::load(d, tu, ru, E, cbase + c4);
+          if (c4 < E4) wp[u][j] = Rows::load(d, tu, ru, E, c4);
         }
       }
     }
@@ -199,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
       if (s + u >= hi) break;
       if (nseg[u]) {
         if (is_first && first_open)
-          store_carry<CPL>(carry, 2 * int64_t(chunk), E, cbase, e4s, rl, LPR, acc);
+          store_carry<CPL>(carry, 2 * int64_t(chunk), E, rl, LPR, acc);
         else
           apply(cur, ct);
         cur = key_of(p[u]);
@@ -222,9 +213,9 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
 
   const bool last_open = knext == cur;  // last segment continues in the next chunk
   if (is_first && (first_open || last_open)) {
-    store_carry<CPL>(carry, 2 * int64_t(chunk), E, cbase, e4s, rl, LPR, acc);
+    store_carry<CPL>(carry, 2 * int64_t(chunk), E, rl, LPR, acc);
   } else if (!is_first && last_open) {
-    store_carry<CPL>(carry, 2 * int64_t(chunk) + 1, E, cbase, e4s, rl, LPR, acc);
+    store_carry<CPL>(carry, 2 * int64_t(chunk) + 1, E, rl, LPR, acc);
   } else {
     apply(cur, ct);
   }
@@ -304,12 +295,12 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
 
 template <class Rows>
 bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
-                int32_t NS, int32_t C, int32_t nchunks, int32_t Q, int32_t cpp, const float* dY,
+                int32_t NS, int32_t C, int32_t nchunks, const float* dY,
                 int32_t B, float inv_b, float lr, double* carry, const int32_t* flags,
                 uint32_t token) {
 #define EMB_SEG(L, CC)                                                                        \
   hipLaunchKernelGGL((segment_sgd<L, CC, Rows>), dim3(blocks), dim3(kBlock), 0, st, d, sorted, \
-                     NS, C, nchunks, Q, cpp, dY, B, inv_b, lr, carry, flags, token)
+                     NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token)
   switch (g.lpr) {
     case 1: EMB_SEG(1, 1); return true;
     case 2: EMB_SEG(2, 1); return true;
@@ -357,17 +348,6 @@ bool launch_fix(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const
 
 }  // namespace
 
-int apply_slices(int dim) {
-  // Slices of 64 columns (256 B of a row) for wide rows: a slice of the dY
-  // rows of one table (B x 256 B, 2 MB at B = 8192) fits one XCD's L2.
-  int q = 1;  // measured on MI355X: slicing trades fabric bytes for issue-bound time
-  (void)dim;
-  if (q < 1) q = 1;
-  if (q > 4) q = 4;
-  while (q > 1 && dim % (4 * q) != 0) --q;
-  return q;
-}
-
 hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
                               float lr, const BwdLayout& L, char* ws, uint32_t token,
                               hipStream_t st) {
@@ -376,21 +356,17 @@ hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const f
   double* carry = reinterpret_cast<double*>(ws + L.off_carry);
   const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
   const float inv_b = 1.0f / float(B);
-  const int Q = apply_slices(d.dim);
-  const RowGeom gs = row_geom(d.dim / Q);
+  const RowGeom gs = row_geom(d.dim);
   const int per_block = kWavesPerBlock * (kWave / gs.lpr);
-  // chunks per part (one part per XCD), a whole number of blocks
-  int64_t cpp = (L.nchunks + kNumXcd - 1) / kNumXcd;
-  cpp = (cpp + per_block - 1) / per_block * per_block;
-  const int blocks_seg = int(kNumXcd * Q * cpp / per_block);
+  const int blocks_seg = int((L.nchunks + per_block - 1) / per_block);
   const RowGeom gf = row_geom(d.dim);
   const int per_block_f = kWavesPerBlock * (kWave / gf.lpr);
   const int blocks_fix = int((L.nchunks + per_block_f - 1) / per_block_f);
   const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
-  bool ok = split ? launch_seg<SplitRows>(gs, blocks_seg, st, d, sorted, NS, C, nch, Q,
-                                          int32_t(cpp), dY, B, inv_b, lr, carry, flags, token)
-                  : launch_seg<Fp32Rows>(gs, blocks_seg, st, d, sorted, NS, C, nch, Q,
-                                         int32_t(cpp), dY, B, inv_b, lr, carry, flags, token);
+  bool ok = split ? launch_seg<SplitRows>(gs, blocks_seg, st, d, sorted, NS, C, nch, dY, B,
+                                          inv_b, lr, carry, flags, token)
+                  : launch_seg<Fp32Rows>(gs, blocks_seg, st, d, sorted, NS, C, nch, dY, B, inv_b,
+                                         lr, carry, flags, token);
   if (ok)
     ok = split ? launch_fix<SplitRows>(gf, blocks_fix, st, d, sorted, NS, C, nch, B, inv_b, lr,
                                        carry, flags, token)
