@@ -126,9 +126,13 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   while (c < 1024 && c * 2 * 16384 <= NS) c *= 2;
   L.chunk = c;
   L.nchunks = (NS + c - 1) / c;
+  // As few passes as digits of at most 10 bits allow, the bits spread evenly
+  // over them (27-bit keys: 3 passes of 9 bits).
   int nbits = 0;
   if (total_rows > 1) nbits = 32 - __builtin_clz(total_rows - 1u);
-  L.passes = (nbits + kRadixBits - 1) / kRadixBits;
+  L.passes = (nbits + kMaxRadixBits - 1) / kMaxRadixBits;
+  L.bits = L.passes > 0 ? (nbits + L.passes - 1) / L.passes : 6;
+  if (L.bits < 6) L.bits = 6;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -137,8 +141,8 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   };
   L.off_a = take(size_t(NS) * 8);
   L.off_b = take(size_t(NS) * 8);
-  L.off_hist = take(size_t(kRadix) * size_t(L.ntiles) * 4);
-  L.off_tot = take(size_t(kRadix) * 4);
+  L.off_hist = take(size_t(kMaxRadix) * size_t(L.ntiles) * 4);
+  L.off_tot = take(size_t(kMaxRadix) * 4);
   L.off_parts = take(size_t(L.nkeyblocks) * 4);
   L.off_flags = take(64);
   L.off_carry = take(for_dedup ? 0 : size_t(2) * size_t(L.nchunks) * size_t(E) * 8);

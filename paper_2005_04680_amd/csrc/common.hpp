@@ -14,9 +14,10 @@ constexpr int kBlock = 256;        // threads per workgroup (4 waves)
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kNumXcd = 8;         // MI355X: 8 XCDs, each with its own L2
 
-// Radix sort geometry: 8-bit digits, 4096-key tiles (256 threads x 16 keys).
-constexpr int kRadixBits = 8;
-constexpr int kRadix = 1 << kRadixBits;
+// Radix sort geometry: digits of 6..10 bits, 4096-key tiles (256 threads x
+// 16 keys).
+constexpr int kMaxRadixBits = 10;
+constexpr int kMaxRadix = 1 << kMaxRadixBits;
 constexpr int kItemsPerThread = 16;
 constexpr int kTile = kBlock * kItemsPerThread;
 
@@ -89,6 +90,7 @@ struct BwdLayout {
   int64_t chunk;       // sorted look-ups per segment-reduce chunk
   int64_t nchunks;
   int passes;          // radix passes
+  int bits;            // digit width of every pass
   size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, total;
 };
 

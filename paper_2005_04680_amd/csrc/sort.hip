@@ -5,11 +5,13 @@
 // A look-up s of bag k (table t = k / B) gets key = rowbase[t] + indices[s];
 // it travels as one 64-bit word (key << 32 | k), so a stable sort on the key
 // bits alone keeps the look-ups of one row in increasing s.  The sort is
-// reduce-then-scan, one pass per 8-bit digit: a per-tile digit histogram, a
-// scan per digit over the tiles, and a scatter in which every 4096-key tile
-// is ranked in LDS (wavefront ballots give each lane its rank among equal
-// digits) and written out in digit order, so that the global stores form
-// runs of consecutive addresses.  No kernel waits on another workgroup.
+// reduce-then-scan, one pass per digit of BITS = 6..10 bits (as few passes as
+// the key width allows: 3 for 27- or 28-bit keys): a per-tile digit
+// histogram, a scan per digit over the tiles, and a scatter in which every
+// 4096-key tile is ranked in LDS (wavefront ballots give each lane its rank
+// among equal digits) and written out in digit order, so that the global
+// stores form runs of consecutive addresses.  No kernel waits on another
+// workgroup.
 #include "common.hpp"
 
 namespace embbag {
@@ -48,21 +50,30 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return before + inc - v;
 }
 
+// Digits handled per thread when a block walks all the digits of a radix.
+template <int BITS>
+struct Radix {
+  static constexpr int R = 1 << BITS;
+  static constexpr int DPT = R > kBlock ? R / kBlock : 1;
+};
+
 // Bags, keys and the first digit's histogram for one tile; offsets checks for
 // a slice of the bags; one status word per block.
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void build_keys(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, float inv_b, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
     uint32_t* __restrict__ hist, int32_t* __restrict__ parts) {
+  constexpr int R = Radix<BITS>::R;
   __shared__ uint32_t lbag[kTile];
-  __shared__ uint32_t lhist[kRadix];
+  __shared__ uint32_t lhist[R];
   __shared__ int32_t lerr;
   __shared__ int32_t krange[2];
   const int tid = threadIdx.x;
   const int blk = blockIdx.x;
   int err = 0;
   if (tid == 0) lerr = 0;
-  lhist[tid] = 0;
+  for (int i = tid; i < R; i += kBlock) lhist[i] = 0;
   __syncthreads();
 
   // Offsets: O[0] == 0, O non-decreasing, O[TB] == NS, all within [0, NS].
@@ -98,6 +109,7 @@ __global__ __launch_bounds__(kBlock) void build_keys(
 #pragma unroll 4
     for (int i = 0; i < kItemsPerThread; ++i) {
       const int s = s_lo + i * kBlock + tid;
+      uint32_t key = 0;
       if (s < s_hi) {
         const uint32_t k = min(lbag[s - s_lo], uint32_t(TB - 1));
         const int t = table_of_bag(k, B, inv_b);
@@ -106,13 +118,13 @@ __global__ __launch_bounds__(kBlock) void build_keys(
           err = min(err, EMBBAG_ERR_INDEX_RANGE);
           r = 0;
         }
-        const uint32_t key = d.rowbase[t] + uint32_t(r);
+        key = d.rowbase[t] + uint32_t(r);
         out[s] = (uint64_t(key) << 32) | k;
-        atomicAdd(&lhist[key & (kRadix - 1)], 1u);
       }
+      if (s < s_hi) atomicAdd(&lhist[key & (R - 1)], 1u);
     }
     __syncthreads();
-    hist[size_t(tid) * ntiles + blk] = lhist[tid];
+    for (int i = tid; i < R; i += kBlock) hist[size_t(i) * ntiles + blk] = lhist[i];
   }
   if (err != 0) atomicMin(&lerr, err);
   __syncthreads();
@@ -120,27 +132,30 @@ __global__ __launch_bounds__(kBlock) void build_keys(
 }
 
 // Digit histogram of one tile of the current arrangement.
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restrict__ src,
                                                         int32_t NS, int shift, int32_t ntiles,
                                                         uint32_t* __restrict__ hist) {
-  __shared__ uint32_t lhist[kRadix];
+  constexpr int R = Radix<BITS>::R;
+  __shared__ uint32_t lhist[R];
   const int tid = threadIdx.x, blk = blockIdx.x;
-  lhist[tid] = 0;
+  for (int i = tid; i < R; i += kBlock) lhist[i] = 0;
   __syncthreads();
   const int base = blk * kTile;
 #pragma unroll 4
   for (int i = 0; i < kItemsPerThread; ++i) {
     const int s = base + i * kBlock + tid;
-    if (s < NS) atomicAdd(&lhist[(key_of(src[s]) >> shift) & (kRadix - 1)], 1u);
+    if (s < NS) atomicAdd(&lhist[(key_of(src[s]) >> shift) & (R - 1)], 1u);
   }
   __syncthreads();
-  hist[size_t(tid) * ntiles + blk] = lhist[tid];
+  for (int i = tid; i < R; i += kBlock) hist[size_t(i) * ntiles + blk] = lhist[i];
 }
 
-// Block d < 256: exclusive scan of digit d's tile counts (in tile order) and
-// the digit total.  Block 256 (first pass only): folds the per-block status
-// words into this call's verdict and lowers the caller's status word.
+// Block d < radix: exclusive scan of digit d's tile counts (in tile order) and
+// the digit total.  Block `radix` (first pass only): folds the per-block
+// status words into this call's verdict and lowers the caller's status word.
 __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist, int32_t ntiles,
+                                                     int32_t radix,
                                                      uint32_t* __restrict__ totals,
                                                      const int32_t* __restrict__ parts,
                                                      int32_t nparts, int32_t* __restrict__ flags,
@@ -149,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   __shared__ int32_t lerr;
   const int tid = threadIdx.x;
-  if (blockIdx.x == kRadix) {
+  if (int(blockIdx.x) == radix) {
     if (tid == 0) lerr = 0;
     __syncthreads();
     int e = 0;
@@ -177,26 +192,41 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
 }
 
 // Stable scatter of one tile by the digit at `shift`.
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void radix_downsweep(
     const uint64_t* __restrict__ src, uint64_t* __restrict__ dst, int32_t NS, int shift,
     int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals) {
+  constexpr int R = Radix<BITS>::R;
+  constexpr int DPT = Radix<BITS>::DPT;
   __shared__ uint64_t buf[kTile];
-  __shared__ uint32_t whist[kWavesPerBlock][kRadix];
-  __shared__ uint32_t lstart[kRadix];
-  __shared__ uint32_t gbase[kRadix];
+  __shared__ uint32_t whist[kWavesPerBlock][R];
+  __shared__ uint32_t lstart[R];
+  __shared__ uint32_t gbase[R];
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   const int tid = threadIdx.x, blk = blockIdx.x;
   const int lane = lane_id();
   const int w = tid / kWave;
 
-  // Global start of each digit's run for this tile.
+  // Global start of each digit's run for this tile (thread tid owns digits
+  // [tid*DPT, tid*DPT + DPT)).
   {
-    uint32_t tot;
-    const uint32_t ex = block_exclusive_scan(totals[tid], scratch, &tot);
-    gbase[tid] = ex + hist[size_t(tid) * ntiles + blk];
-  }
+    uint32_t v[DPT], sum = 0;
 #pragma unroll
-  for (int i = 0; i < kWavesPerBlock; ++i) whist[i][tid] = 0;
+    for (int i = 0; i < DPT; ++i) {
+      const int dg = tid * DPT + i;
+      v[i] = dg < R ? totals[dg] : 0u;
+      sum += v[i];
+    }
+    uint32_t tot;
+    uint32_t ex = block_exclusive_scan(sum, scratch, &tot);
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int dg = tid * DPT + i;
+      if (dg < R) gbase[dg] = ex + hist[size_t(dg) * ntiles + blk];
+      ex += v[i];
+    }
+  }
+  for (int i = tid; i < kWavesPerBlock * R; i += kBlock) (&whist[0][0])[i] = 0;
   __syncthreads();
 
   // Wave w owns keys [w*1024, (w+1)*1024) of the tile, item i of lane l being
@@ -214,11 +244,11 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
 #pragma unroll
   for (int i = 0; i < kItemsPerThread; ++i) {
     const bool valid = wbase + i * kWave + lane < NS;
-    const uint32_t dg = (key_of(item[i]) >> shift) & (kRadix - 1);
+    const uint32_t dg = (key_of(item[i]) >> shift) & (R - 1);
     dig[i] = dg;
     uint64_t peers = __builtin_amdgcn_ballot_w64(valid);
 #pragma unroll
-    for (int b = 0; b < kRadixBits; ++b) {
+    for (int b = 0; b < BITS; ++b) {
       const bool bit = (dg >> b) & 1u;
       const uint64_t m = __builtin_amdgcn_ballot_w64(bit);
       peers &= bit ? m : ~m;
@@ -233,15 +263,30 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   {
     // Per digit: offsets of each wave's run inside the tile's digit run, and
     // the start of each digit's run in the locally sorted tile.
-    uint32_t run = 0;
+    uint32_t run[DPT], sum = 0;
 #pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
-      const uint32_t c = whist[i][tid];
-      whist[i][tid] = run;
-      run += c;
+    for (int i = 0; i < DPT; ++i) {
+      const int dg = tid * DPT + i;
+      uint32_t r = 0;
+      if (dg < R) {
+#pragma unroll
+        for (int ww = 0; ww < kWavesPerBlock; ++ww) {
+          const uint32_t c = whist[ww][dg];
+          whist[ww][dg] = r;
+          r += c;
+        }
+      }
+      run[i] = r;
+      sum += r;
     }
     uint32_t tot;
-    lstart[tid] = block_exclusive_scan(run, scratch, &tot);
+    uint32_t ex = block_exclusive_scan(sum, scratch, &tot);
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int dg = tid * DPT + i;
+      if (dg < R) lstart[dg] = ex;
+      ex += run[i];
+    }
   }
   __syncthreads();
 #pragma unroll
@@ -252,7 +297,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   const int nvalid = min(kTile, NS - blk * kTile);
   for (int j = tid; j < nvalid; j += kBlock) {
     const uint64_t it = buf[j];
-    const uint32_t dg = (key_of(it) >> shift) & (kRadix - 1);
+    const uint32_t dg = (key_of(it) >> shift) & (R - 1);
     dst[gbase[dg] + (j - lstart[dg])] = it;
   }
 }
@@ -330,11 +375,11 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
   }
 }
 
-}  // namespace
-
-hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
+template <int BITS>
+hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
                        uint32_t token, hipStream_t st) {
+  constexpr int R = Radix<BITS>::R;
   const int32_t TB = d.num_tables * B;
   uint64_t* a = reinterpret_cast<uint64_t*>(ws + L.off_a);
   uint64_t* b = reinterpret_cast<uint64_t*>(ws + L.off_b);
@@ -346,31 +391,46 @@ hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const in
   const int vb = (TB + 1 + nkb - 1) / nkb;
   const int ntiles = int(L.ntiles);
   const float inv_b = B > 0 ? 1.0f / float(B) : 0.0f;
-  hipLaunchKernelGGL(build_keys, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B, inv_b,
-                     TB, ntiles, vb, a, hist, parts);
-  // Status verdict (block 256 of the first scan, or alone when nothing is sorted).
+  hipLaunchKernelGGL(build_keys<BITS>, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B,
+                     inv_b, TB, ntiles, vb, a, hist, parts);
+  // Status verdict (block R of the first scan, or alone when nothing is sorted).
   const int passes = NS > 0 ? L.passes : 0;
   if (passes == 0) {
-    hipLaunchKernelGGL(radix_scan, dim3(kRadix + 1), dim3(kBlock), 0, st, hist, 0, totals, parts,
+    hipLaunchKernelGGL(radix_scan, dim3(R + 1), dim3(kBlock), 0, st, hist, 0, R, totals, parts,
                        nkb, flags, d_status, token);
     return hipGetLastError();
   }
   uint64_t* src = a;
   uint64_t* dst = b;
   for (int p = 0; p < passes; ++p) {
-    const int shift = p * kRadixBits;
+    const int shift = p * BITS;
     if (p > 0)
-      hipLaunchKernelGGL(radix_upsweep, dim3(ntiles), dim3(kBlock), 0, st, src, int32_t(NS),
-                         shift, ntiles, hist);
-    hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? kRadix + 1 : kRadix), dim3(kBlock), 0, st, hist,
-                       ntiles, totals, parts, nkb, flags, d_status, token);
-    hipLaunchKernelGGL(radix_downsweep, dim3(ntiles), dim3(kBlock), 0, st, src, dst,
+      hipLaunchKernelGGL(radix_upsweep<BITS>, dim3(ntiles), dim3(kBlock), 0, st, src,
+                         int32_t(NS), shift, ntiles, hist);
+    hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? R + 1 : R), dim3(kBlock), 0, st, hist, ntiles, R,
+                       totals, parts, nkb, flags, d_status, token);
+    hipLaunchKernelGGL(radix_downsweep<BITS>, dim3(ntiles), dim3(kBlock), 0, st, src, dst,
                        int32_t(NS), shift, ntiles, hist, totals);
     uint64_t* tmp = src;
     src = dst;
     dst = tmp;
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
+                       int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
+                       uint32_t token, hipStream_t st) {
+  switch (L.bits) {
+    case 6: return sort_passes<6>(d, B, I, O, NS, L, ws, d_status, token, st);
+    case 7: return sort_passes<7>(d, B, I, O, NS, L, ws, d_status, token, st);
+    case 8: return sort_passes<8>(d, B, I, O, NS, L, ws, d_status, token, st);
+    case 9: return sort_passes<9>(d, B, I, O, NS, L, ws, d_status, token, st);
+    case 10: return sort_passes<10>(d, B, I, O, NS, L, ws, d_status, token, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
