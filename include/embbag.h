@@ -115,6 +115,30 @@ int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* 
                         const embbag_tables_t* tables, void* workspace, size_t workspace_bytes,
                         int32_t* d_status, hipStream_t stream);
 
+/* Pooling modes of the *_pooled entry points (Section II: L = A^T W, where
+ * column n of A holds a weight a_p for every row bag n reads). */
+#define EMBBAG_POOL_SUM 0  /* Y[k] = sum over s of a_s * W[I[s]] (a_s = 1 without weights) */
+#define EMBBAG_POOL_MEAN 1 /* Y[k] = (sum over s of W[I[s]]) / |bag k|; empty bag -> +0.0 */
+
+/* Forward with per-look-up weights or mean pooling.  `per_sample_weights` is
+ * a device FP32 array [num_indices] (one weight per look-up, nullable; only
+ * with EMBBAG_POOL_SUM).  With null weights and EMBBAG_POOL_SUM this is
+ * embbag_forward.  An invalid (weights, pooling) pair is EMBBAG_ERR_INVALID_ARG. */
+int embbag_forward_pooled(const embbag_tables_t* tables, int32_t batch, const int32_t* indices,
+                          const int32_t* offsets, int64_t num_indices,
+                          const float* per_sample_weights, int32_t pooling, float* pooled_out,
+                          int32_t* d_status, hipStream_t stream);
+
+/* The matching fused backward + SGD: every touched row r of table t gets
+ *   W[r] -= lr * sum over its look-ups s of c_s * grad_pooled[bag(s)],
+ * c_s = a_s (weighted sum), 1 (sum) or 1/|bag(s)| (mean), once per row, the
+ * sum in FP64.  Same workspace as embbag_backward_sgd. */
+int embbag_backward_sgd_pooled(const float* grad_pooled, int32_t batch, const int32_t* indices,
+                               const int32_t* offsets, int64_t num_indices,
+                               const float* per_sample_weights, int32_t pooling, float lr,
+                               const embbag_tables_t* tables, void* workspace,
+                               size_t workspace_bytes, int32_t* d_status, hipStream_t stream);
+
 /* The fused backward in two phases, for callers that overlap its integer
  * work with other parts of a training step.  embbag_backward_sgd(...) is
  * exactly embbag_backward_prepare(...) followed by embbag_backward_apply_sgd(...).

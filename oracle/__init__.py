@@ -47,13 +47,16 @@ def lib():
         L.oracle_backward_sgd.argtypes = [p, i32, i32, i32, p, p, p, p, i64, f32]
         L.oracle_backward_sgd_literal.argtypes = [p, i32, i32, i32, p, p, p, p, i64, f32]
         L.oracle_backward_sgd_split.argtypes = [p, i32, i32, i32, p, p, p, p, p, i64, f32]
+        L.oracle_forward_weighted.argtypes = [i32, i32, i32, p, p, p, p, i64, p, i32, p]
+        L.oracle_backward_sgd_weighted.argtypes = [p, i32, i32, i32, p, p, p, p, i64, p, i32, f32]
         L.oracle_split.argtypes = [p, p, p, i64]
         L.oracle_combine.argtypes = [p, p, p, i64]
         L.oracle_split_roundtrip_mismatches.argtypes = [C.c_uint64, C.c_uint64]
         L.oracle_split_roundtrip_mismatches.restype = i64
         for name in ("oracle_validate", "oracle_forward", "oracle_forward_literal",
                      "oracle_forward_split", "oracle_dedup", "oracle_backward_sgd",
-                     "oracle_backward_sgd_literal", "oracle_backward_sgd_split"):
+                     "oracle_backward_sgd_literal", "oracle_backward_sgd_split",
+                     "oracle_forward_weighted", "oracle_backward_sgd_weighted"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -155,6 +158,35 @@ def backward_sgd_split(grad, batch: int, indices, offsets, lr: float, hi_tables,
     rows = _rows(hi_tables)
     return lib().oracle_backward_sgd_split(_ptr(G), T, batch, E, _ptr(rows), _ptr_array(hi_tables),
                                            _ptr_array(lo_tables), _ptr(I), _ptr(O), I.size, lr)
+
+
+POOL_SUM = 0
+POOL_MEAN = 1
+
+
+def forward_weighted(tables, batch: int, indices, offsets, weights=None, mode: int = POOL_SUM):
+    """Weighted-sum (per-look-up weights) or mean pooling.  Returns (status, pooled)."""
+    tables = [_c(t, np.float32) for t in tables]
+    I, O = _c(indices, np.int32), _c(offsets, np.int32)
+    a = None if weights is None else _c(weights, np.float32)
+    T, E = len(tables), tables[0].shape[1]
+    rows = _rows(tables)
+    Y = np.zeros((T, batch, E), dtype=np.float32)
+    rc = lib().oracle_forward_weighted(T, batch, E, _ptr(rows), _ptr_array(tables), _ptr(I),
+                                       _ptr(O), I.size, _ptr(a), mode, _ptr(Y))
+    return rc, Y
+
+
+def backward_sgd_weighted(grad, batch: int, indices, offsets, lr: float, tables, weights=None,
+                          mode: int = POOL_SUM) -> int:
+    tables = [_c(t, np.float32) for t in tables]
+    G = _c(grad, np.float32)
+    I, O = _c(indices, np.int32), _c(offsets, np.int32)
+    a = None if weights is None else _c(weights, np.float32)
+    T, E = len(tables), tables[0].shape[1]
+    rows = _rows(tables)
+    return lib().oracle_backward_sgd_weighted(_ptr(G), T, batch, E, _ptr(rows), _ptr_array(tables),
+                                              _ptr(I), _ptr(O), I.size, _ptr(a), mode, lr)
 
 
 def split(w):

@@ -138,6 +138,7 @@ struct Dedup {
   std::vector<int64_t> rowbase;
   std::vector<uint32_t> key, bag, sorted_key, sorted_bag, unique_key;
   std::vector<int32_t> seg_off;
+  std::vector<int64_t> perm;  // look-up position s of each sorted entry
 };
 
 void dedup_impl(int32_t T, int32_t B, const int64_t* rows, const int32_t* I, const int32_t* O,
@@ -155,6 +156,7 @@ void dedup_impl(int32_t T, int32_t B, const int64_t* rows, const int32_t* I, con
   std::iota(perm.begin(), perm.end(), int64_t(0));
   std::stable_sort(perm.begin(), perm.end(),
                    [&](int64_t a, int64_t b) { return d.key[a] < d.key[b]; });
+  d.perm = perm;
   d.sorted_key.resize(NS);
   d.sorted_bag.resize(NS);
   for (int64_t i = 0; i < NS; ++i) {
@@ -342,6 +344,69 @@ int oracle_backward_sgd_literal(const float* dY, int32_t T, int32_t B, int32_t E
         w[e] = w[e] + step;
       }
     }
+  return kOk;
+}
+
+// ---- Weighted and mean pooling (Section II's general L = A^T W) ----------
+// Column n of A holds a weight a_p for every row bag n reads.  With weights
+// `a` (one per look-up; null means all ones) and sum pooling,
+//   Y[k] = sum over s in bag k of a[s] * W_t[I[s]];
+// mean pooling (mode 1, no weights) divides each bag's sum by its number of
+// look-ups (an empty bag stays +0.0).  The backward is the transpose: row r
+// of table t receives sum over its look-ups s of c_s * dY[bag(s)], with
+// c_s = a[s] (sum) or 1 / |bag(s)| (mean), applied once with SGD.
+constexpr int kPoolSum = 0;
+constexpr int kPoolMean = 1;
+
+int oracle_forward_weighted(int32_t T, int32_t B, int32_t E, const int64_t* rows,
+                            const float* const* W, const int32_t* I, const int32_t* O, int64_t NS,
+                            const float* a, int32_t mode, float* Y) {
+  if (W == nullptr || (mode != kPoolSum && mode != kPoolMean) || (mode == kPoolMean && a))
+    return kErrInvalidArg;
+  int rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
+  std::vector<double> acc(E);
+  for (int64_t k = 0; k < int64_t(T) * B; ++k) {
+    const int t = int(k / B);
+    std::fill(acc.begin(), acc.end(), 0.0);
+    for (int64_t s = O[k]; s < O[k + 1]; ++s) {
+      const double c = a ? double(a[s]) : 1.0;
+      for (int e = 0; e < E; ++e) acc[e] += c * double(W[t][int64_t(I[s]) * E + e]);
+    }
+    const int64_t n = O[k + 1] - O[k];
+    for (int e = 0; e < E; ++e)
+      Y[k * E + e] = float(mode == kPoolMean && n > 0 ? acc[e] / double(n) : acc[e]);
+  }
+  return kOk;
+}
+
+int oracle_backward_sgd_weighted(const float* dY, int32_t T, int32_t B, int32_t E,
+                                 const int64_t* rows, float* const* W, const int32_t* I,
+                                 const int32_t* O, int64_t NS, const float* a, int32_t mode,
+                                 float lr) {
+  if (W == nullptr || (mode != kPoolSum && mode != kPoolMean) || (mode == kPoolMean && a))
+    return kErrInvalidArg;
+  int rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
+  if (dY == nullptr && NS > 0) return kErrInvalidArg;
+  Dedup d;
+  dedup_impl(T, B, rows, I, O, NS, d);
+  std::vector<double> acc(E);
+  for (size_t u = 0; u < d.unique_key.size(); ++u) {
+    std::fill(acc.begin(), acc.end(), 0.0);
+    for (int64_t i = d.seg_off[u]; i < d.seg_off[u + 1]; ++i) {
+      const int64_t s = d.perm[i];
+      const int64_t k = d.sorted_bag[i];
+      double c = 1.0;
+      if (a) c = double(a[s]);
+      if (mode == kPoolMean) c = 1.0 / double(O[k + 1] - O[k]);
+      const float* g = dY + k * E;
+      for (int e = 0; e < E; ++e) acc[e] += c * double(g[e]);
+    }
+    const int t = table_of_key(d, d.unique_key[u]);
+    float* w = W[t] + (int64_t(d.unique_key[u]) - d.rowbase[t]) * E;
+    for (int e = 0; e < E; ++e) w[e] = float(double(w[e]) - double(lr) * acc[e]);
+  }
   return kOk;
 }
 

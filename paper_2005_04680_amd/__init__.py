@@ -24,6 +24,8 @@ EMBBAG_ERR_WORKSPACE = -2
 EMBBAG_ERR_INDEX_RANGE = -3
 EMBBAG_ERR_OFFSETS = -4
 EMBBAG_ERR_HIP = -5
+EMBBAG_POOL_SUM = 0
+EMBBAG_POOL_MEAN = 1
 
 
 class EmbbagError(RuntimeError):
@@ -63,6 +65,9 @@ def lib():
         L.embbag_backward_workspace_bytes.restype = sz
         L.embbag_backward_sgd.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz, p, p]
         L.embbag_backward_sgd_split_bf16.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz, p, p]
+        L.embbag_forward_pooled.argtypes = [p, i32, p, p, i64, p, i32, p, p, p]
+        L.embbag_backward_sgd_pooled.argtypes = [p, i32, p, p, i64, p, i32, C.c_float, p, p, sz,
+                                                 p, p]
         L.embbag_backward_prepare.argtypes = [i32, p, i32, i32, p, p, i64, p, sz, p, p]
         L.embbag_backward_apply_sgd.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
         L.embbag_backward_apply_sgd_split_bf16.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
@@ -74,6 +79,7 @@ def lib():
         L.embbag_status_read.argtypes = [p, p]
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
                   "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
+                  "embbag_forward_pooled", "embbag_backward_sgd_pooled",
                   "embbag_backward_apply_sgd", "embbag_backward_apply_sgd_split_bf16",
                   "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
                   "embbag_status_read"):
@@ -159,6 +165,30 @@ def embbag_forward(weights, batch, indices, offsets, pooled_out, d_status=None, 
                                 _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
                                 _ptr(pooled_out, _dt("float32"), "pooled_out"),
                                 _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_forward_pooled(weights, batch, indices, offsets, pooled_out, per_sample_weights=None,
+                          pooling=EMBBAG_POOL_SUM, d_status=None, stream=None) -> int:
+    """Weighted-sum (one weight per look-up) or mean pooling over FP32 tables."""
+    s, keep = _tables_struct(weights)
+    return lib().embbag_forward_pooled(C.byref(s), int(batch), _ptr(indices, _dt(*_I32), "indices"),
+                                       _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
+                                       _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"),
+                                       int(pooling), _ptr(pooled_out, _dt("float32"), "pooled_out"),
+                                       _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_sgd_pooled(grad_pooled, batch, indices, offsets, lr, weights, workspace,
+                               per_sample_weights=None, pooling=EMBBAG_POOL_SUM, d_status=None,
+                               stream=None) -> int:
+    s, keep = _tables_struct(weights)
+    return lib().embbag_backward_sgd_pooled(
+        _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
+        _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
+        int(indices.numel()), _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"),
+        int(pooling), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
+        int(workspace.numel() * workspace.element_size()), _ptr(d_status, _dt(*_I32), "d_status"),
+        _stream(stream))
 
 
 def embbag_forward_split_bf16(hi, batch, indices, offsets, pooled_out, d_status=None,

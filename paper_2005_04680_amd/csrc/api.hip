@@ -55,28 +55,38 @@ int check_bags(int32_t T, int32_t B, const int32_t* I, const int32_t* O, int64_t
 
 int hip_status(hipError_t e) { return e == hipSuccess ? EMBBAG_OK : EMBBAG_ERR_HIP; }
 
+// Pooling from the public (weights, pooling) pair; -1 if the pair is invalid
+// (weights are defined for sum pooling only).
+int pool_mode(const float* weights, int32_t pooling) {
+  if (pooling == EMBBAG_POOL_SUM) return weights ? kPoolWeighted : kPoolPlain;
+  if (pooling == EMBBAG_POOL_MEAN && weights == nullptr) return kPoolMean;
+  return -1;
+}
+
 int forward_common(const TableDesc& d, bool split, int32_t B, const int32_t* I, const int32_t* O,
-                   int64_t NS, float* Y, int32_t* d_status, hipStream_t st) {
+                   int64_t NS, float* Y, int32_t* d_status, const PoolArgs& pool,
+                   hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
   if (int64_t(d.num_tables) * B > 0 && (Y == nullptr || !aligned(Y, 16)))
     return EMBBAG_ERR_INVALID_ARG;
-  return hip_status(launch_forward(d, split, B, I, O, NS, Y, d_status, st));
+  return hip_status(launch_forward(d, split, B, I, O, NS, Y, d_status, pool, st));
 }
 
 int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O, int64_t NS,
-                   void* ws, size_t ws_bytes, int32_t* d_status, hipStream_t st) {
+                   void* ws, size_t ws_bytes, int32_t* d_status, int mode, hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
   const uint32_t total = d.rowbase[d.num_tables];
   const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
   if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
   return hip_status(launch_sort(d, B, I, O, NS, L, static_cast<char*>(ws), d_status,
-                                phase_token(d.num_tables, B, NS, total), st));
+                                phase_token(d.num_tables, B, NS, total, mode),
+                                mode == kPoolWeighted, st));
 }
 
 int apply_common(const TableDesc& d, bool split, const float* dY, int32_t B, int64_t NS, float lr,
-                 void* ws, size_t ws_bytes, hipStream_t st) {
+                 void* ws, size_t ws_bytes, const PoolArgs& pool, hipStream_t st) {
   if (B < 0 || NS < 0 || NS > kInt32Max || int64_t(d.num_tables) * B + 1 > kInt32Max)
     return EMBBAG_ERR_INVALID_ARG;
   if (int64_t(d.num_tables) * B == 0 && NS > 0) return EMBBAG_ERR_OFFSETS;
@@ -85,27 +95,32 @@ int apply_common(const TableDesc& d, bool split, const float* dY, int32_t B, int
   const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
   if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
   return hip_status(launch_segment_sgd(d, split, B, dY, lr, L, static_cast<char*>(ws),
-                                       phase_token(d.num_tables, B, NS, total), st));
+                                       phase_token(d.num_tables, B, NS, total, pool.mode), pool,
+                                       st));
 }
 
 int backward_common(const TableDesc& d, bool split, const float* dY, int32_t B, const int32_t* I,
                     const int32_t* O, int64_t NS, float lr, void* ws, size_t ws_bytes,
-                    int32_t* d_status, hipStream_t st) {
+                    int32_t* d_status, const PoolArgs& pool, hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
   if (NS > 0 && (dY == nullptr || !aligned(dY, 16))) return EMBBAG_ERR_INVALID_ARG;
-  rc = prepare_common(d, B, I, O, NS, ws, ws_bytes, d_status, st);
+  if (pool.mode == kPoolWeighted && NS > 0 && pool.weights == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  rc = prepare_common(d, B, I, O, NS, ws, ws_bytes, d_status, pool.mode, st);
   if (rc) return rc;
-  return apply_common(d, split, dY, B, NS, lr, ws, ws_bytes, st);
+  return apply_common(d, split, dY, B, NS, lr, ws, ws_bytes, pool, st);
 }
 
 }  // namespace
 
 namespace embbag {
 
-uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows) {
+uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows, int mode) {
+  // The weighted payload (look-up positions) differs from the others (bags).
+  const uint64_t payload = mode == kPoolWeighted ? 1u : 0u;
   uint64_t h = 0x243F6A8885A308D3ull;
-  for (uint64_t v : {uint64_t(uint32_t(T)), uint64_t(uint32_t(B)), uint64_t(NS), uint64_t(total_rows)}) {
+  for (uint64_t v : {uint64_t(uint32_t(T)), uint64_t(uint32_t(B)), uint64_t(NS),
+                     uint64_t(total_rows), payload}) {
     h ^= v + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
     h *= 0xBF58476D1CE4E5B9ull;
   }
@@ -147,6 +162,7 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   L.off_flags = take(64);
   L.off_carry = take(for_dedup ? 0 : size_t(2) * size_t(L.nchunks) * size_t(E) * 8);
   L.off_uniq = take(for_dedup ? size_t(L.ntiles) * 4 : 0);
+  L.off_bagof = take(for_dedup ? 0 : size_t(NS) * 4);
   L.total = off;
   return L;
 }
@@ -176,7 +192,26 @@ int embbag_forward(const embbag_tables_t* tables, int32_t batch, const int32_t* 
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
   return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, d_status,
-                        stream);
+                        PoolArgs{}, stream);
+}
+
+int embbag_forward_pooled(const embbag_tables_t* tables, int32_t batch, const int32_t* indices,
+                          const int32_t* offsets, int64_t num_indices,
+                          const float* per_sample_weights, int32_t pooling, float* pooled_out,
+                          int32_t* d_status, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  const int mode = pool_mode(per_sample_weights, pooling);
+  if (mode < 0) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  PoolArgs pool;
+  pool.mode = mode;
+  pool.weights = per_sample_weights;
+  pool.offsets = offsets;
+  return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, d_status,
+                        pool, stream);
 }
 
 int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch,
@@ -189,7 +224,7 @@ int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch
                      reinterpret_cast<void* const*>(tables->hi), nullptr, 8, &d);
   if (rc) return rc;
   return forward_common(d, true, batch, indices, offsets, num_indices, pooled_out, d_status,
-                        stream);
+                        PoolArgs{}, stream);
 }
 
 size_t embbag_backward_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices,
@@ -211,7 +246,27 @@ int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* 
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
   return backward_common(d, false, grad_pooled, batch, indices, offsets, num_indices, lr,
-                         workspace, workspace_bytes, d_status, stream);
+                         workspace, workspace_bytes, d_status, PoolArgs{}, stream);
+}
+
+int embbag_backward_sgd_pooled(const float* grad_pooled, int32_t batch, const int32_t* indices,
+                               const int32_t* offsets, int64_t num_indices,
+                               const float* per_sample_weights, int32_t pooling, float lr,
+                               const embbag_tables_t* tables, void* workspace,
+                               size_t workspace_bytes, int32_t* d_status, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  const int mode = pool_mode(per_sample_weights, pooling);
+  if (mode < 0) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  PoolArgs pool;
+  pool.mode = mode;
+  pool.weights = per_sample_weights;
+  pool.offsets = offsets;
+  return backward_common(d, false, grad_pooled, batch, indices, offsets, num_indices, lr,
+                         workspace, workspace_bytes, d_status, pool, stream);
 }
 
 int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
@@ -227,7 +282,7 @@ int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
                      reinterpret_cast<void* const*>(tables->lo), 8, &d);
   if (rc) return rc;
   return backward_common(d, true, grad_pooled, batch, indices, offsets, num_indices, lr,
-                         workspace, workspace_bytes, d_status, stream);
+                         workspace, workspace_bytes, d_status, PoolArgs{}, stream);
 }
 
 int embbag_backward_prepare(int32_t num_tables, const int64_t* rows, int32_t dim, int32_t batch,
@@ -238,7 +293,7 @@ int embbag_backward_prepare(int32_t num_tables, const int64_t* rows, int32_t dim
   int rc = make_desc(num_tables, dim, rows, nullptr, nullptr, 0, &d);
   if (rc) return rc;
   return prepare_common(d, batch, indices, offsets, num_indices, workspace, workspace_bytes,
-                        d_status, stream);
+                        d_status, kPoolPlain, stream);
 }
 
 int embbag_backward_apply_sgd(const float* grad_pooled, int32_t batch, int64_t num_indices,
@@ -250,7 +305,7 @@ int embbag_backward_apply_sgd(const float* grad_pooled, int32_t batch, int64_t n
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
   return apply_common(d, false, grad_pooled, batch, num_indices, lr, workspace, workspace_bytes,
-                      stream);
+                      PoolArgs{}, stream);
 }
 
 int embbag_backward_apply_sgd_split_bf16(const float* grad_pooled, int32_t batch,
@@ -264,7 +319,7 @@ int embbag_backward_apply_sgd_split_bf16(const float* grad_pooled, int32_t batch
                      reinterpret_cast<void* const*>(tables->lo), 8, &d);
   if (rc) return rc;
   return apply_common(d, true, grad_pooled, batch, num_indices, lr, workspace, workspace_bytes,
-                      stream);
+                      PoolArgs{}, stream);
 }
 
 int embbag_split_fp32(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t stream) {
@@ -305,8 +360,8 @@ int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const i
     return EMBBAG_ERR_WORKSPACE;
   char* w = static_cast<char*>(workspace);
   if (launch_sort(d, batch, indices, offsets, num_indices, L, w, d_status,
-                  phase_token(num_tables, batch, num_indices, d.rowbase[num_tables]),
-                  stream) != hipSuccess)
+                  phase_token(num_tables, batch, num_indices, d.rowbase[num_tables], kPoolPlain),
+                  false, stream) != hipSuccess)
     return EMBBAG_ERR_HIP;
   return hip_status(launch_unique(sorted_buffer(L, w), L, w, sorted_keys, sorted_bags,
                                   unique_keys, seg_off, d_num_unique, stream));

@@ -82,6 +82,16 @@ __device__ __forceinline__ int table_of_bag(uint32_t k, int B, float inv_b) {
 __device__ __forceinline__ uint32_t key_of(uint64_t p) { return uint32_t(p >> 32); }
 __device__ __forceinline__ uint32_t bag_of(uint64_t p) { return uint32_t(p); }
 
+// Pooling of a bag (Section II's L = A^T W): plain sum (Algorithm 1), sum
+// weighted by one weight per look-up, or mean (sum / number of look-ups).
+enum PoolMode : int { kPoolPlain = 0, kPoolWeighted = 1, kPoolMean = 2 };
+
+struct PoolArgs {
+  int mode = kPoolPlain;
+  const float* weights = nullptr;   // kPoolWeighted: [num_indices]
+  const int32_t* offsets = nullptr; // kPoolMean: bag sizes for the backward
+};
+
 // ---- launchers (host) ------------------------------------------------------
 struct BwdLayout {
   int64_t ns;
@@ -91,15 +101,16 @@ struct BwdLayout {
   int64_t nchunks;
   int passes;          // radix passes
   int bits;            // digit width of every pass
-  size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, total;
+  size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, off_bagof,
+      total;
 };
 
 BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
                           bool for_dedup);
 
 // Stamp the sort phase leaves in the workspace for the apply phase: a hash of
-// the sizes the sorted look-ups belong to (never 0).
-uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows);
+// the sizes the sorted look-ups belong to and of their payload (never 0).
+uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows, int mode);
 
 // The buffer that holds the sorted look-ups after the sort phase.
 inline uint64_t* sorted_buffer(const BwdLayout& L, char* ws) {
@@ -109,16 +120,18 @@ inline uint64_t* sorted_buffer(const BwdLayout& L, char* ws) {
 
 hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
                           const int32_t* O, int64_t NS, float* Y, int32_t* status,
-                          hipStream_t st);
+                          const PoolArgs& pool, hipStream_t st);
 
 // Builds keys, validates, sorts into sorted_buffer(L, ws); stamps `token`.
+// The payload of a sorted word is the bag, or (by_lookup) the look-up
+// position s, with bag[s] then kept in the workspace.
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       uint32_t token, hipStream_t st);
+                       uint32_t token, bool by_lookup, hipStream_t st);
 
 hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
                               float lr, const BwdLayout& L, char* ws, uint32_t token,
-                              hipStream_t st);
+                              const PoolArgs& pool, hipStream_t st);
 
 hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
                          uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,

@@ -31,11 +31,11 @@ __device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, int E, i
   }
 }
 
-template <int LPR, int CPL, bool SPLIT, bool MULTI>
+template <int LPR, int CPL, bool SPLIT, bool MULTI, int MODE>
 __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, int32_t G, int32_t groups_per_table, int32_t items, float* __restrict__ Y,
-    int32_t* __restrict__ status) {
+    int32_t* __restrict__ status, const float* __restrict__ A) {
   constexpr int R = kWave / LPR;
   constexpr int U = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
   const int E = d.dim;
@@ -54,12 +54,17 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   const void* base = d.w[t];
   int err = 0;
 
-  auto store_bag = [&](int k, const f4* acc) {
+  // Stores bag k's pooled row; mean pooling divides by the bag's n look-ups.
+  auto store_bag = [&](int k, const f4* acc, int n) {
     float* y = Y + size_t(k) * E;
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
       const int c4 = rl + j * LPR;
-      if (c4 < E4) *reinterpret_cast<f4*>(y + c4 * 4) = acc[j];
+      f4 v = acc[j];
+      if constexpr (MODE == kPoolMean) {
+        if (n > 0) v = v / float(n);
+      }
+      if (c4 < E4) *reinterpret_cast<f4*>(y + c4 * 4) = v;
     }
   };
 
@@ -68,6 +73,7 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   bool bad = s0 < 0 || s1 > NS || s0 > s1;
   int k = k0;
   int bound = s1;
+  int bstart = s0;  // first look-up of bag k
   if constexpr (MULTI) {
     bound = bad ? 0 : O[k0 + 1];
     bad = bad || bound < s0 || bound > s1;
@@ -85,10 +91,15 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   // load is valid, and such slots are masked out of the sum.
   constexpr bool kWin = LPR >= U;
   int wbase = s0, vcur = 0, vnext = 0;
+  float acur = 0.f, anext = 0.f;  // per-look-up weights, same windows
   if constexpr (kWin) {
     if (!bad) {
       vcur = s0 + rl < s1 ? I[s0 + rl] : 0;
       vnext = s0 + LPR + rl < s1 ? I[s0 + LPR + rl] : 0;
+      if constexpr (MODE == kPoolWeighted) {
+        acur = s0 + rl < s1 ? A[s0 + rl] : 0.f;
+        anext = s0 + LPR + rl < s1 ? A[s0 + LPR + rl] : 0.f;
+      }
     }
   }
 
@@ -98,21 +109,31 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
         wbase += LPR;
         vcur = vnext;
         vnext = wbase + LPR + rl < s1 ? I[wbase + LPR + rl] : 0;
+        if constexpr (MODE == kPoolWeighted) {
+          acur = anext;
+          anext = wbase + LPR + rl < s1 ? A[wbase + LPR + rl] : 0.f;
+        }
       }
     }
     f4 v[U][CPL];
     bool use[U];
+    float wt[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int ss = min(s + u, s1 - 1);
       int idx;
       if constexpr (kWin) {
-        if constexpr (LPR == kWave)
+        if constexpr (LPR == kWave) {
           idx = __builtin_amdgcn_readlane(vcur, ss - wbase);
-        else
+          if constexpr (MODE == kPoolWeighted)
+            wt[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(acur), ss - wbase));
+        } else {
           idx = __shfl(vcur, rg * LPR + (ss - wbase), kWave);
+          if constexpr (MODE == kPoolWeighted) wt[u] = __shfl(acur, rg * LPR + (ss - wbase), kWave);
+        }
       } else {
         idx = I[ss];
+        if constexpr (MODE == kPoolWeighted) wt[u] = A[ss];
       }
       const bool ok = uint32_t(idx) < M;
       if (!ok) err = min(err, EMBBAG_ERR_INDEX_RANGE);
@@ -132,7 +153,8 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
         // Crossing the end of bag k (and of any empty bags after it).  While
         // ss < s1 = O[k1] and O is non-decreasing up to s1, k + 1 < k1 here.
         while (ss >= bound) {
-          store_bag(k, acc);
+          store_bag(k, acc, bound - bstart);
+          bstart = bound;
 #pragma unroll
           for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
           ++k;
@@ -146,18 +168,23 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
         if (bad) break;
       }
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) acc[j] = use[u] ? acc[j] + v[u][j] : acc[j];
+      for (int j = 0; j < CPL; ++j) {
+        if constexpr (MODE == kPoolWeighted)
+          acc[j] = use[u] ? acc[j] + wt[u] * v[u][j] : acc[j];
+        else
+          acc[j] = use[u] ? acc[j] + v[u][j] : acc[j];
+      }
     }
   }
   if (!bad) {
-    store_bag(k, acc);
+    store_bag(k, acc, s1 - bstart);
     if constexpr (MULTI) {
       // Remaining bags of the group hold no look-ups: O[k'] == s1 for them all.
       for (int kk = k + 1; kk < k1; ++kk) {
         if (O[kk] != s1) bad = true;
 #pragma unroll
         for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-        store_bag(kk, acc);
+        store_bag(kk, acc, 0);
       }
     }
   }
@@ -172,23 +199,24 @@ __global__ void fwd_empty_check(const int32_t* __restrict__ O, int32_t NS,
     atomicMin(status, EMBBAG_ERR_OFFSETS);
 }
 
-template <bool SPLIT, int LPR, int CPL>
+template <bool SPLIT, int MODE, int LPR, int CPL>
 void launch_one(dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I, const int32_t* O,
                 int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items, float* Y,
-                int32_t* status) {
+                int32_t* status, const float* A) {
   if (G > 1)
-    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, true>), grid, dim3(kBlock), 0, st, d, I, O,
-                       NS, B, G, gpt, items, Y, status);
+    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, true, MODE>), grid, dim3(kBlock), 0, st, d,
+                       I, O, NS, B, G, gpt, items, Y, status, A);
   else
-    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, false>), grid, dim3(kBlock), 0, st, d, I,
-                       O, NS, B, G, gpt, items, Y, status);
+    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, false, MODE>), grid, dim3(kBlock), 0, st,
+                       d, I, O, NS, B, G, gpt, items, Y, status, A);
 }
 
-template <bool SPLIT>
+template <bool SPLIT, int MODE>
 bool dispatch(RowGeom g, dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I,
               const int32_t* O, int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items,
-              float* Y, int32_t* status) {
-#define EMB_FWD(L, C) launch_one<SPLIT, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status)
+              float* Y, int32_t* status, const float* A) {
+#define EMB_FWD(L, C) \
+  launch_one<SPLIT, MODE, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status, A)
   switch (g.lpr) {
     case 1: EMB_FWD(1, 1); return true;
     case 2: EMB_FWD(2, 1); return true;
@@ -212,7 +240,7 @@ bool dispatch(RowGeom g, dim3 grid, hipStream_t st, const TableDesc& d, const in
 
 hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
                           const int32_t* O, int64_t NS, float* Y, int32_t* status,
-                          hipStream_t st) {
+                          const PoolArgs& pool, hipStream_t st) {
   const int64_t TB = int64_t(d.num_tables) * B;
   if (TB == 0) {
     hipLaunchKernelGGL(fwd_empty_check, dim3(1), dim3(kWave), 0, st, O, int32_t(NS), status);
@@ -229,10 +257,17 @@ hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32
   const RowGeom g = row_geom(d.dim);
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const dim3 grid(unsigned((items + per_block - 1) / per_block));
-  const bool ok = split ? dispatch<true>(g, grid, st, d, I, O, int32_t(NS), B, G, gpt,
-                                         int32_t(items), Y, status)
-                        : dispatch<false>(g, grid, st, d, I, O, int32_t(NS), B, G, gpt,
-                                          int32_t(items), Y, status);
+  const int32_t ns = int32_t(NS), it = int32_t(items);
+  bool ok = false;
+  if (split)
+    ok = dispatch<true, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
+  else if (pool.mode == kPoolWeighted)
+    ok = dispatch<false, kPoolWeighted>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status,
+                                        pool.weights);
+  else if (pool.mode == kPoolMean)
+    ok = dispatch<false, kPoolMean>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
+  else
+    ok = dispatch<false, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();
 }

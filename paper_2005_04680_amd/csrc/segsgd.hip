@@ -92,11 +92,33 @@ __device__ __forceinline__ void store_carry(double* carry, int64_t slot, int E, 
   }
 }
 
-template <int LPR, int CPL, class Rows>
+// Look-up coefficients of the gradient sum (Section II's weights a_p): 1 for
+// plain sums, the look-up's weight for weighted sums (the sorted payload is
+// then the look-up position s, and bagof[s] its bag), 1/|bag| for means.
+struct PoolDev {
+  const uint32_t* bagof;
+  const float* weights;
+  const int32_t* offsets;
+};
+
+template <int MODE>
+__device__ __forceinline__ uint32_t bag_at(uint64_t p, const PoolDev& pd) {
+  if constexpr (MODE == kPoolWeighted) return pd.bagof[bag_of(p)];
+  return bag_of(p);
+}
+
+template <int MODE>
+__device__ __forceinline__ double coef_at(uint64_t p, uint32_t bag, const PoolDev& pd) {
+  if constexpr (MODE == kPoolWeighted) return double(pd.weights[bag_of(p)]);
+  if constexpr (MODE == kPoolMean) return 1.0 / double(pd.offsets[bag + 1] - pd.offsets[bag]);
+  return 1.0;
+}
+
+template <int LPR, int CPL, class Rows, int MODE>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     const float* __restrict__ dY, int32_t B, float inv_b, float lr,
-    double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token) {
+    double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
   // A data error, or no sort result for these sizes: no table writes.
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
@@ -117,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   const uint32_t knext = hi < NS ? key_of(sorted[hi]) : kNoKey;
   const uint64_t p0 = sorted[lo];
   uint32_t cur = key_of(p0);
-  int ct = table_of_bag(bag_of(p0), B, inv_b);
+  int ct = table_of_bag(bag_at<MODE>(p0, pd), B, inv_b);
   const bool first_open = kprev == cur;  // first segment began in an earlier chunk
   bool is_first = true;
 
@@ -152,6 +174,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   uint64_t plast = p0;  // look-up before the current group (none before lo: p0 itself)
   for (int s = lo; s < hi; s += U) {
     uint64_t p[U];
+    uint32_t bg[U];
     bool dup[U], nseg[U];
     f4 g[U][CPL];
     typename Rows::Pre wp[U][CPL];
@@ -164,8 +187,10 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
       nseg[u] = valid && key_of(p[u]) != key_of(pq);
     }
 #pragma unroll
+    for (int u = 0; u < U; ++u) bg[u] = s + u < hi ? bag_at<MODE>(p[u], pd) : 0u;
+#pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float* gy = dY + size_t(bag_of(p[u])) * E;
+      const float* gy = dY + size_t(bg[u]) * E;
       const bool ld = s + u < hi && !dup[u];
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
@@ -174,7 +199,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
                                    : f4{0.f, 0.f, 0.f, 0.f};
       }
       if (nseg[u]) {
-        const int tu = table_of_bag(bag_of(p[u]), B, inv_b);
+        const int tu = table_of_bag(bg[u], B, inv_b);
         const uint32_t ru = key_of(p[u]) - d.rowbase[tu];
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
@@ -194,7 +219,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
         else
           apply(cur, ct);
         cur = key_of(p[u]);
-        ct = table_of_bag(bag_of(p[u]), B, inv_b);
+        ct = table_of_bag(bg[u], B, inv_b);
         is_first = false;
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
@@ -202,10 +227,15 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
           pre[j] = wp[u][j];
         }
       }
+      double c = 1.0;
+      if constexpr (MODE != kPoolPlain) c = coef_at<MODE>(p[u], bg[u], pd);
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         if (!dup[u]) glast[j] = g[u][j];
-        acc[j] += widen(glast[j]);
+        if constexpr (MODE == kPoolPlain)
+          acc[j] += widen(glast[j]);
+        else
+          acc[j] += c * widen(glast[j]);
       }
     }
     plast = p[U - 1];
@@ -223,11 +253,11 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
 
 // Segments that cross chunk boundaries: the chunk where one begins sums the
 // partials in chunk order and applies the row.
-template <int LPR, int CPL, class Rows>
+template <int LPR, int CPL, class Rows, int MODE>
 __global__ __launch_bounds__(kBlock) void segment_fixup(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     int32_t B, float inv_b, float lr, const double* __restrict__ carry,
-    const int32_t* __restrict__ flags, uint32_t token) {
+    const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
   constexpr int UF = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
@@ -242,7 +272,7 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   if (key_of(sorted[hi]) != kl) return;             // last segment ends here
   const uint32_t kf = key_of(sorted[lo]);
   if (kf == kl && lo > 0 && key_of(sorted[lo - 1]) == kl) return;  // began earlier
-  const int ct = table_of_bag(bag_of(sorted[hi - 1]), B, inv_b);
+  const int ct = table_of_bag(bag_at<MODE>(sorted[hi - 1], pd), B, inv_b);
   const uint32_t r = kl - d.rowbase[ct];
   const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
 
@@ -293,14 +323,13 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   }
 }
 
-template <class Rows>
+template <class Rows, int MODE>
 bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
-                int32_t NS, int32_t C, int32_t nchunks, const float* dY,
-                int32_t B, float inv_b, float lr, double* carry, const int32_t* flags,
-                uint32_t token) {
-#define EMB_SEG(L, CC)                                                                        \
-  hipLaunchKernelGGL((segment_sgd<L, CC, Rows>), dim3(blocks), dim3(kBlock), 0, st, d, sorted, \
-                     NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token)
+                int32_t NS, int32_t C, int32_t nchunks, const float* dY, int32_t B, float inv_b,
+                float lr, double* carry, const int32_t* flags, uint32_t token, PoolDev pd) {
+#define EMB_SEG(L, CC)                                                                     \
+  hipLaunchKernelGGL((segment_sgd<L, CC, Rows, MODE>), dim3(blocks), dim3(kBlock), 0, st, d, \
+                     sorted, NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token, pd)
   switch (g.lpr) {
     case 1: EMB_SEG(1, 1); return true;
     case 2: EMB_SEG(2, 1); return true;
@@ -320,13 +349,13 @@ bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const
   return false;
 }
 
-template <class Rows>
+template <class Rows, int MODE>
 bool launch_fix(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
                 int32_t NS, int32_t C, int32_t nchunks, int32_t B, float inv_b, float lr,
-                const double* carry, const int32_t* flags, uint32_t token) {
-#define EMB_FIX(L, CC)                                                                          \
-  hipLaunchKernelGGL((segment_fixup<L, CC, Rows>), dim3(blocks), dim3(kBlock), 0, st, d, sorted, \
-                     NS, C, nchunks, B, inv_b, lr, carry, flags, token)
+                const double* carry, const int32_t* flags, uint32_t token, PoolDev pd) {
+#define EMB_FIX(L, CC)                                                                       \
+  hipLaunchKernelGGL((segment_fixup<L, CC, Rows, MODE>), dim3(blocks), dim3(kBlock), 0, st, d, \
+                     sorted, NS, C, nchunks, B, inv_b, lr, carry, flags, token, pd)
   switch (g.lpr) {
     case 1: EMB_FIX(1, 1); return true;
     case 2: EMB_FIX(2, 1); return true;
@@ -346,32 +375,39 @@ bool launch_fix(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const
   return false;
 }
 
-}  // namespace
-
-hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
-                              float lr, const BwdLayout& L, char* ws, uint32_t token,
-                              hipStream_t st) {
-  if (L.ns == 0) return hipSuccess;
+template <class Rows, int MODE>
+bool launch_apply(const TableDesc& d, int32_t B, const float* dY, float lr, const BwdLayout& L,
+                  char* ws, uint32_t token, PoolDev pd, hipStream_t st) {
   const uint64_t* sorted = sorted_buffer(L, ws);
   double* carry = reinterpret_cast<double*>(ws + L.off_carry);
   const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
   const float inv_b = 1.0f / float(B);
-  const RowGeom gs = row_geom(d.dim);
-  const int per_block = kWavesPerBlock * (kWave / gs.lpr);
-  const int blocks_seg = int((L.nchunks + per_block - 1) / per_block);
-  const RowGeom gf = row_geom(d.dim);
-  const int per_block_f = kWavesPerBlock * (kWave / gf.lpr);
-  const int blocks_fix = int((L.nchunks + per_block_f - 1) / per_block_f);
+  const RowGeom g = row_geom(d.dim);
+  const int per_block = kWavesPerBlock * (kWave / g.lpr);
+  const int blocks = int((L.nchunks + per_block - 1) / per_block);
   const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
-  bool ok = split ? launch_seg<SplitRows>(gs, blocks_seg, st, d, sorted, NS, C, nch, dY, B,
-                                          inv_b, lr, carry, flags, token)
-                  : launch_seg<Fp32Rows>(gs, blocks_seg, st, d, sorted, NS, C, nch, dY, B, inv_b,
-                                         lr, carry, flags, token);
-  if (ok)
-    ok = split ? launch_fix<SplitRows>(gf, blocks_fix, st, d, sorted, NS, C, nch, B, inv_b, lr,
-                                       carry, flags, token)
-               : launch_fix<Fp32Rows>(gf, blocks_fix, st, d, sorted, NS, C, nch, B, inv_b, lr,
-                                      carry, flags, token);
+  return launch_seg<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, dY, B, inv_b, lr, carry,
+                                flags, token, pd) &&
+         launch_fix<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry, flags,
+                                token, pd);
+}
+
+}  // namespace
+
+hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
+                              float lr, const BwdLayout& L, char* ws, uint32_t token,
+                              const PoolArgs& pool, hipStream_t st) {
+  if (L.ns == 0) return hipSuccess;
+  PoolDev pd{reinterpret_cast<const uint32_t*>(ws + L.off_bagof), pool.weights, pool.offsets};
+  bool ok;
+  if (split)
+    ok = launch_apply<SplitRows, kPoolPlain>(d, B, dY, lr, L, ws, token, pd, st);
+  else if (pool.mode == kPoolWeighted)
+    ok = launch_apply<Fp32Rows, kPoolWeighted>(d, B, dY, lr, L, ws, token, pd, st);
+  else if (pool.mode == kPoolMean)
+    ok = launch_apply<Fp32Rows, kPoolMean>(d, B, dY, lr, L, ws, token, pd, st);
+  else
+    ok = launch_apply<Fp32Rows, kPoolPlain>(d, B, dY, lr, L, ws, token, pd, st);
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -63,7 +63,7 @@ template <int BITS>
 __global__ __launch_bounds__(kBlock) void build_keys(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, float inv_b, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
-    uint32_t* __restrict__ hist, int32_t* __restrict__ parts) {
+    uint32_t* __restrict__ hist, int32_t* __restrict__ parts, uint32_t* __restrict__ bagof) {
   constexpr int R = Radix<BITS>::R;
   __shared__ uint32_t lbag[kTile];
   __shared__ uint32_t lhist[R];
@@ -119,7 +119,12 @@ __global__ __launch_bounds__(kBlock) void build_keys(
           r = 0;
         }
         key = d.rowbase[t] + uint32_t(r);
-        out[s] = (uint64_t(key) << 32) | k;
+        if (bagof != nullptr) {  // payload = look-up position, bag kept aside
+          out[s] = (uint64_t(key) << 32) | uint32_t(s);
+          bagof[s] = k;
+        } else {
+          out[s] = (uint64_t(key) << 32) | k;
+        }
       }
       if (s < s_hi) atomicAdd(&lhist[key & (R - 1)], 1u);
     }
@@ -378,7 +383,7 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
 template <int BITS>
 hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       uint32_t token, hipStream_t st) {
+                       uint32_t token, bool by_lookup, hipStream_t st) {
   constexpr int R = Radix<BITS>::R;
   const int32_t TB = d.num_tables * B;
   uint64_t* a = reinterpret_cast<uint64_t*>(ws + L.off_a);
@@ -391,8 +396,9 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   const int vb = (TB + 1 + nkb - 1) / nkb;
   const int ntiles = int(L.ntiles);
   const float inv_b = B > 0 ? 1.0f / float(B) : 0.0f;
+  uint32_t* bagof = by_lookup ? reinterpret_cast<uint32_t*>(ws + L.off_bagof) : nullptr;
   hipLaunchKernelGGL(build_keys<BITS>, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B,
-                     inv_b, TB, ntiles, vb, a, hist, parts);
+                     inv_b, TB, ntiles, vb, a, hist, parts, bagof);
   // Status verdict (block R of the first scan, or alone when nothing is sorted).
   const int passes = NS > 0 ? L.passes : 0;
   if (passes == 0) {
@@ -422,13 +428,13 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
 
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       uint32_t token, hipStream_t st) {
+                       uint32_t token, bool by_lookup, hipStream_t st) {
   switch (L.bits) {
-    case 6: return sort_passes<6>(d, B, I, O, NS, L, ws, d_status, token, st);
-    case 7: return sort_passes<7>(d, B, I, O, NS, L, ws, d_status, token, st);
-    case 8: return sort_passes<8>(d, B, I, O, NS, L, ws, d_status, token, st);
-    case 9: return sort_passes<9>(d, B, I, O, NS, L, ws, d_status, token, st);
-    case 10: return sort_passes<10>(d, B, I, O, NS, L, ws, d_status, token, st);
+    case 6: return sort_passes<6>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 7: return sort_passes<7>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 8: return sort_passes<8>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 9: return sort_passes<9>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 10: return sort_passes<10>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
   }
   return hipErrorInvalidValue;
 }

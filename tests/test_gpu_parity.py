@@ -339,3 +339,57 @@ def test_apply_needs_a_prepared_workspace():
         assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
         for a, b in zip(gt.host(), before):
             assert bits_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# Weighted-sum and mean pooling (Section II's weights a_p)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dim", [16, 64, 128, 256, 1024])
+@pytest.mark.parametrize("mode", ["weighted", "mean"])
+@pytest.mark.parametrize("maxp", [3, 40])
+def test_weighted_and_mean(dim, mode, maxp):
+    import paper_2005_04680_amd as pk
+    rng = np.random.default_rng(dim * 3 + maxp + (mode == "mean"))
+    rows = (700, 40, 3000)
+    batch = 61
+    W = _tables(rng, rows, dim, 0.05)
+    I, O = random_bags(rng, rows, batch, maxp, empty_frac=0.1, hot_frac=0.3)
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    a = rng.uniform(-2, 2, I.size).astype(np.float32) if mode == "weighted" else None
+    pool = pk.EMBBAG_POOL_MEAN if mode == "mean" else pk.EMBBAG_POOL_SUM
+    om = oracle.POOL_MEAN if mode == "mean" else oracle.POOL_SUM
+    log(f"[pooled] {mode} dim={dim} maxp={maxp} NS={I.size}")
+    gt = GpuTables(W)
+    Id, Od, Gd = to_dev(I), to_dev(O), to_dev(G)
+    ad = None if a is None else to_dev(a)
+    Y = torch.empty((len(rows), batch, dim), dtype=torch.float32, device=DEV)
+    assert pk.embbag_forward_pooled(gt.w, batch, Id, Od, Y, ad, pool, gt.status) == 0
+    rc, Yref = oracle.forward_weighted(W, batch, I, O, a, om)
+    assert rc == 0
+    assert_close(Y.cpu().numpy(), Yref, f"{mode} pooled")
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(len(rows), batch, I.size, dim),
+                     dtype=torch.uint8, device=DEV)
+    assert pk.embbag_backward_sgd_pooled(Gd, batch, Id, Od, 0.1, gt.w, ws, ad, pool, gt.status) == 0
+    assert gt.read_status() == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd_weighted(G, batch, I, O, 0.1, Wref, a, om) == 0
+    for t, (wg, wr) in enumerate(zip(gt.host(), Wref)):
+        assert_close(wg, wr, f"{mode} table {t}")
+    # a weighted workspace is not taken for a plain apply
+    if mode == "weighted":
+        before = gt.host()
+        assert pk.embbag_backward_apply_sgd(Gd, batch, I.size, 0.1, gt.w, ws) == 0
+        for x, y in zip(gt.host(), before):
+            assert bits_equal(x, y)
+
+
+def test_pooled_argument_errors():
+    import paper_2005_04680_amd as pk
+    W = [np.ones((8, 16), np.float32)]
+    gt = GpuTables(W)
+    I = to_dev(np.array([1, 2], np.int32))
+    O = to_dev(np.array([0, 1, 2], np.int32))
+    a = to_dev(np.ones(2, np.float32))
+    Y = torch.empty((1, 2, 16), dtype=torch.float32, device=DEV)
+    assert pk.embbag_forward_pooled(gt.w, 2, I, O, Y, a, pk.EMBBAG_POOL_MEAN) == pk.EMBBAG_ERR_INVALID_ARG
+    assert pk.embbag_forward_pooled(gt.w, 2, I, O, Y, None, 7) == pk.EMBBAG_ERR_INVALID_ARG

@@ -403,3 +403,80 @@ def test_split_update_equals_fp32_update(oracle):
     assert oracle.backward_sgd(G, 9, I, O, 0.1, W1) == oracle.OK
     for h, l, w in zip(hi, lo, W1):
         assert np.array_equal(oracle.combine(h, l).view(np.uint32), w.view(np.uint32))
+
+
+# ----------------------------------------------------------------------------
+# weighted and mean pooling (Section II's L = A^T W with weights a_p)
+# ----------------------------------------------------------------------------
+def _dense_A_weighted(rows_t, batch, t, indices, offsets, weights=None, mean=False):
+    A = np.zeros((batch, rows_t), dtype=np.float64)
+    for b in range(batch):
+        k = t * batch + b
+        n = offsets[k + 1] - offsets[k]
+        for s in range(offsets[k], offsets[k + 1]):
+            c = 1.0 if weights is None else float(weights[s])
+            if mean:
+                c /= n
+            A[b, indices[s]] += c
+    return A
+
+
+@pytest.mark.parametrize("case", CASES)
+@pytest.mark.parametrize("mode", ["weighted", "mean"])
+def test_weighted_and_mean_match_dense_and_torch(oracle, case, mode):
+    rows, dim, batch, maxp, ef, hf, seed = case
+    rng = np.random.default_rng(seed + 500)
+    W = _tables(rng, rows, dim)
+    I, O = random_bags(rng, rows, batch, maxp, ef, hf)
+    a = rng.uniform(-2, 2, I.size).astype(np.float32) if mode == "weighted" else None
+    m = oracle.POOL_MEAN if mode == "mean" else oracle.POOL_SUM
+    rc, Y = oracle.forward_weighted(W, batch, I, O, a, m)
+    assert rc == oracle.OK
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    W1 = [w.copy() for w in W]
+    assert oracle.backward_sgd_weighted(G, batch, I, O, 0.1, W1, a, m) == oracle.OK
+    for t in range(len(rows)):
+        A = _dense_A_weighted(rows[t], batch, t, I, O, a, mode == "mean")
+        assert _ulp_close(Y[t], (A @ W[t].astype(np.float64)).astype(np.float32), ulps=1)
+        grad = A.T @ G[t].astype(np.float64)
+        touched = np.zeros(rows[t], bool)
+        touched[I[O[t * batch]:O[(t + 1) * batch]]] = True
+        ref = W[t].astype(np.float64) - np.float64(np.float32(0.1)) * grad
+        assert _ulp_close(W1[t][touched], ref[touched].astype(np.float32), ulps=1)
+        assert np.array_equal(W1[t][~touched].view(np.uint32), W[t][~touched].view(np.uint32))
+        # library routine
+        lo, hi = O[t * batch], O[(t + 1) * batch]
+        idx = torch.from_numpy(I[lo:hi].astype(np.int64))
+        offs = torch.from_numpy((O[t * batch:(t + 1) * batch] - lo).astype(np.int64))
+        psw = None if a is None else torch.from_numpy(a[lo:hi])
+        ref_t = torch.nn.functional.embedding_bag(idx, torch.from_numpy(W[t]), offs,
+                                                  mode="mean" if mode == "mean" else "sum",
+                                                  per_sample_weights=psw)
+        np.testing.assert_allclose(Y[t], ref_t.numpy(), rtol=RTOL, atol=ATOL)
+
+
+def test_weighted_special_cases(oracle):
+    rng = np.random.default_rng(31)
+    rows, dim, batch = (40, 25), 8, 7
+    W = _tables(rng, rows, dim)
+    I, O = random_bags(rng, rows, batch, 6, 0.2, 0.3)
+    # unit weights reproduce the plain sum bit for bit
+    rc, Y1 = oracle.forward_weighted(W, batch, I, O, np.ones(I.size, np.float32))
+    rc2, Y0 = oracle.forward(W, batch, I, O)
+    assert rc == rc2 == 0 and np.array_equal(Y1.view(np.uint32), Y0.view(np.uint32))
+    G = rng.standard_normal((2, batch, dim)).astype(np.float32)
+    Wa, Wb = [w.copy() for w in W], [w.copy() for w in W]
+    assert oracle.backward_sgd_weighted(G, batch, I, O, 0.1, Wa, np.ones(I.size, np.float32)) == 0
+    assert oracle.backward_sgd(G, batch, I, O, 0.1, Wb) == 0
+    for a_, b_ in zip(Wa, Wb):
+        assert np.array_equal(a_.view(np.uint32), b_.view(np.uint32))
+    # mean of n copies of one row is that row; an empty bag is +0.0
+    I2 = np.array([3, 3, 3, 5], np.int32)
+    O2 = np.array([0, 3, 3, 4], np.int32)
+    rc, Ym = oracle.forward_weighted([W[0]], 3, I2, O2, None, oracle.POOL_MEAN)
+    assert rc == 0
+    assert np.array_equal(Ym[0, 0], W[0][3]) and np.array_equal(Ym[0, 2], W[0][5])
+    assert np.array_equal(Ym[0, 1].view(np.uint32), np.zeros(dim, np.uint32))
+    # weights with mean pooling are rejected (torch allows weights with sum only)
+    assert oracle.forward_weighted(W, batch, I, O, np.ones(I.size, np.float32),
+                                   oracle.POOL_MEAN)[0] == oracle.ERR_INVALID_ARG
