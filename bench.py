@@ -123,6 +123,40 @@ def cpu_baseline(cfg, batch_I, G, sample_bags):
                        f"forward + fused backward/SGD, single-threaded, {dt:.2f} s")}
 
 
+def time_baselines(pk, torch, cfg, tables, batches, stream, reps=3):
+    """Average ms per step of the unfused designs, same workload and stream."""
+    T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
+    dW = torch.empty((NS, E), dtype=torch.float32, device=tables[0].device)
+    res = {}
+
+    def timed(fn, n):
+        fn(batches[0])  # warm-up
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(n):
+            fn(batches[i % len(batches)])
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return round(ev0.elapsed_time(ev1) / n, 4)
+
+    res["alg2_materialize_ms"] = timed(
+        lambda bt: pk.check(pk.embbag_baseline_materialize(bt["G"], T, B, E, bt["O"], NS, dW)), reps)
+    res["alg3_atomic_update_ms"] = timed(
+        lambda bt: pk.check(pk.embbag_baseline_update_atomic(dW, B, bt["I"], bt["O"], cfg.lr,
+                                                             tables)), reps)
+    res["alg2_3_fused_atomic_ms"] = timed(
+        lambda bt: pk.check(pk.embbag_baseline_backward_sgd_atomic(bt["G"], B, bt["I"], bt["O"],
+                                                                   cfg.lr, tables)), reps)
+    res["alg4_owner_update_ms"] = timed(
+        lambda bt: pk.check(pk.embbag_baseline_update_owner(dW, B, bt["I"], bt["O"], cfg.lr,
+                                                            tables, 256)), 1)
+    res["note"] = ("unfused = alg2 + alg3 (or alg2 + alg4); the fused sort-and-segment backward "
+                   "is bwd_prepare_ms + bwd_apply_ms")
+    del dW
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -137,6 +171,10 @@ def main():
     ap.add_argument("--overlap-prepare", action="store_true",
                     help="run the backward's index phase on a second stream, overlapped with "
                          "the forward (measured slower on MI355X: both are memory-bound)")
+    ap.add_argument("--baselines", action="store_true",
+                    help="also time the paper's unfused update designs on the GPU: Algorithm 2 "
+                         "(materialised dW) + Algorithm 3 (FP32 atomics), the fused atomic update, "
+                         "and Algorithm 4 (row-range ownership, 256 owners)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE to bytes)")
@@ -322,6 +360,8 @@ def main():
         "wall_s_timed": round(wall, 3),
         "roofline": roof,
     }
+    if args.baselines and not split:
+        out["baselines"] = time_baselines(pk, torch, cfg, tables, batches, main)
     if not args.no_cpu_baseline:
         b0 = batches[0]
         out["cpu_baseline"] = cpu_baseline(cfg, b0["I_host"], b0["G_host"], args.cpu_sample_bags)

@@ -214,6 +214,41 @@ int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const i
                  int32_t* d_num_unique, void* workspace, size_t workspace_bytes,
                  int32_t* d_status, hipStream_t stream);
 
+/* ---- Baselines: the paper's unfused update designs on the GPU -------------
+ * For measurement against the fused backward; not needed to train.  The
+ * atomic variants add in a scheduling-dependent FP32 order (results vary in
+ * the last bits between runs); the owner variant is deterministic.  Indices
+ * out of range are skipped (and reported through the nullable d_status);
+ * offsets must be valid. */
+
+/* Algorithm 2: dW[s][:] = grad_pooled[bag(s)][:], dW a device FP32 array
+ * [num_indices][dim] (NS x E: 13.4 GB at 13.1M look-ups of E = 256). */
+int embbag_baseline_materialize(const float* grad_pooled, int32_t num_tables, int32_t batch,
+                                int32_t dim, const int32_t* offsets, int64_t num_indices,
+                                float* dW, int32_t* d_status, hipStream_t stream);
+
+/* Algorithm 3 with hardware FP32 atomics: W_t[I[s]][:] += (-lr) * dW[s][:]. */
+int embbag_baseline_update_atomic(const float* dW, int32_t batch, const int32_t* indices,
+                                  const int32_t* offsets, int64_t num_indices, float lr,
+                                  const embbag_tables_t* tables, int32_t* d_status,
+                                  hipStream_t stream);
+
+/* Algorithms 2+3 fused with atomics: W_t[I[s]][:] += (-lr) * grad_pooled[bag(s)][:]. */
+int embbag_baseline_backward_sgd_atomic(const float* grad_pooled, int32_t batch,
+                                        const int32_t* indices, const int32_t* offsets,
+                                        int64_t num_indices, float lr,
+                                        const embbag_tables_t* tables, int32_t* d_status,
+                                        hipStream_t stream);
+
+/* Algorithm 4, race-free by row ownership: `owners` wavefronts each own an
+ * equal range of the global row space (tables concatenated), scan all
+ * look-ups and apply W[row] += (-lr) * dW[s] for their own rows in increasing
+ * s, in FP32 (the order and precision of a sequential loop over s). */
+int embbag_baseline_update_owner(const float* dW, int32_t batch, const int32_t* indices,
+                                 const int32_t* offsets, int64_t num_indices, float lr,
+                                 const embbag_tables_t* tables, int32_t owners,
+                                 hipStream_t stream);
+
 /* Waits for `stream` and returns the device status word (*d_status), or
  * EMBBAG_ERR_HIP if the wait or copy fails. */
 int embbag_status_read(const int32_t* d_status, hipStream_t stream);

@@ -76,12 +76,18 @@ def lib():
         L.embbag_dedup_workspace_bytes.argtypes = [i32, i32, i64]
         L.embbag_dedup_workspace_bytes.restype = sz
         L.embbag_dedup.argtypes = [i32, p, i32, p, p, i64, p, p, p, p, p, p, sz, p, p]
+        L.embbag_baseline_materialize.argtypes = [p, i32, i32, i32, p, i64, p, p, p]
+        L.embbag_baseline_update_atomic.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
+        L.embbag_baseline_backward_sgd_atomic.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
+        L.embbag_baseline_update_owner.argtypes = [p, i32, p, p, i64, C.c_float, p, i32, p]
         L.embbag_status_read.argtypes = [p, p]
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
                   "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
                   "embbag_forward_pooled", "embbag_backward_sgd_pooled",
                   "embbag_backward_apply_sgd", "embbag_backward_apply_sgd_split_bf16",
                   "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
+                  "embbag_baseline_materialize", "embbag_baseline_update_atomic",
+                  "embbag_baseline_backward_sgd_atomic", "embbag_baseline_update_owner",
                   "embbag_status_read"):
             getattr(L, n).restype = C.c_int
         _lib = L
@@ -292,6 +298,48 @@ def embbag_dedup(rows, batch, indices, offsets, sorted_keys, sorted_bags, unique
                               _ptr(workspace, None, "workspace"),
                               int(workspace.numel() * workspace.element_size()),
                               _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+# ---- baselines: the paper's unfused designs (for measurement) --------------
+def embbag_baseline_materialize(grad_pooled, num_tables, batch, dim, offsets, num_indices, dW,
+                                d_status=None, stream=None) -> int:
+    return lib().embbag_baseline_materialize(_ptr(grad_pooled, _dt("float32"), "grad_pooled"),
+                                             int(num_tables), int(batch), int(dim),
+                                             _ptr(offsets, _dt(*_I32), "offsets"),
+                                             int(num_indices), _ptr(dW, _dt("float32"), "dW"),
+                                             _ptr(d_status, _dt(*_I32), "d_status"),
+                                             _stream(stream))
+
+
+def embbag_baseline_update_atomic(dW, batch, indices, offsets, lr, weights, d_status=None,
+                                  stream=None) -> int:
+    s, keep = _tables_struct(weights)
+    return lib().embbag_baseline_update_atomic(_ptr(dW, _dt("float32"), "dW"), int(batch),
+                                               _ptr(indices, _dt(*_I32), "indices"),
+                                               _ptr(offsets, _dt(*_I32), "offsets"),
+                                               int(indices.numel()), float(lr), C.byref(s),
+                                               _ptr(d_status, _dt(*_I32), "d_status"),
+                                               _stream(stream))
+
+
+def embbag_baseline_backward_sgd_atomic(grad_pooled, batch, indices, offsets, lr, weights,
+                                        d_status=None, stream=None) -> int:
+    s, keep = _tables_struct(weights)
+    return lib().embbag_baseline_backward_sgd_atomic(
+        _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
+        _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
+        int(indices.numel()), float(lr), C.byref(s), _ptr(d_status, _dt(*_I32), "d_status"),
+        _stream(stream))
+
+
+def embbag_baseline_update_owner(dW, batch, indices, offsets, lr, weights, owners,
+                                 stream=None) -> int:
+    s, keep = _tables_struct(weights)
+    return lib().embbag_baseline_update_owner(_ptr(dW, _dt("float32"), "dW"), int(batch),
+                                              _ptr(indices, _dt(*_I32), "indices"),
+                                              _ptr(offsets, _dt(*_I32), "offsets"),
+                                              int(indices.numel()), float(lr), C.byref(s),
+                                              int(owners), _stream(stream))
 
 
 def embbag_status_read(d_status, stream=None) -> int:

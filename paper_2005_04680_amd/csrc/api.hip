@@ -367,6 +367,70 @@ int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const i
                                   unique_keys, seg_off, d_num_unique, stream));
 }
 
+int embbag_baseline_materialize(const float* grad_pooled, int32_t num_tables, int32_t batch,
+                                int32_t dim, const int32_t* offsets, int64_t num_indices,
+                                float* dW, int32_t* d_status, hipStream_t stream) {
+  if (num_tables < 1 || num_tables > kMaxTables || dim < 4 || dim > 1024 || dim % 4 != 0)
+    return EMBBAG_ERR_INVALID_ARG;
+  int rc = check_bags(num_tables, batch, nullptr, offsets, 0);
+  if (rc) return rc;
+  if (num_indices < 0 || num_indices > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+  if (int64_t(num_tables) * batch > 0 && (grad_pooled == nullptr || !aligned(grad_pooled, 16)))
+    return EMBBAG_ERR_INVALID_ARG;
+  if (num_indices > 0 && (dW == nullptr || !aligned(dW, 16))) return EMBBAG_ERR_INVALID_ARG;
+  return hip_status(
+      launch_materialize(grad_pooled, offsets, num_indices, num_tables, batch, dim, dW, d_status,
+                         stream));
+}
+
+static int baseline_update(const float* src, bool fused, int32_t batch, const int32_t* indices,
+                           const int32_t* offsets, int64_t num_indices, float lr,
+                           const embbag_tables_t* tables, int32_t* d_status, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  rc = check_bags(d.num_tables, batch, indices, offsets, num_indices);
+  if (rc) return rc;
+  if (num_indices > 0 && (src == nullptr || !aligned(src, 16))) return EMBBAG_ERR_INVALID_ARG;
+  return hip_status(launch_atomic_update(d, src, fused, indices, offsets, num_indices, batch, lr,
+                                         d_status, stream));
+}
+
+int embbag_baseline_update_atomic(const float* dW, int32_t batch, const int32_t* indices,
+                                  const int32_t* offsets, int64_t num_indices, float lr,
+                                  const embbag_tables_t* tables, int32_t* d_status,
+                                  hipStream_t stream) {
+  return baseline_update(dW, false, batch, indices, offsets, num_indices, lr, tables, d_status,
+                         stream);
+}
+
+int embbag_baseline_backward_sgd_atomic(const float* grad_pooled, int32_t batch,
+                                        const int32_t* indices, const int32_t* offsets,
+                                        int64_t num_indices, float lr,
+                                        const embbag_tables_t* tables, int32_t* d_status,
+                                        hipStream_t stream) {
+  return baseline_update(grad_pooled, true, batch, indices, offsets, num_indices, lr, tables,
+                         d_status, stream);
+}
+
+int embbag_baseline_update_owner(const float* dW, int32_t batch, const int32_t* indices,
+                                 const int32_t* offsets, int64_t num_indices, float lr,
+                                 const embbag_tables_t* tables, int32_t owners,
+                                 hipStream_t stream) {
+  if (tables == nullptr || owners < 1 || owners > 65536) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  rc = check_bags(d.num_tables, batch, indices, offsets, num_indices);
+  if (rc) return rc;
+  if (num_indices > 0 && (dW == nullptr || !aligned(dW, 16))) return EMBBAG_ERR_INVALID_ARG;
+  return hip_status(
+      launch_owner_update(d, dW, indices, offsets, num_indices, batch, owners, lr, stream));
+}
+
 int embbag_status_read(const int32_t* d_status, hipStream_t stream) {
   if (d_status == nullptr) return EMBBAG_ERR_INVALID_ARG;
   if (hipStreamSynchronize(stream) != hipSuccess) return EMBBAG_ERR_HIP;

@@ -137,6 +137,16 @@ hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
                          uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,
                          int32_t* seg_off, int32_t* d_num_unique, hipStream_t st);
 
+// Baselines: the paper's unfused designs (Algorithms 2, 3, 4) on the GPU.
+hipError_t launch_materialize(const float* dY, const int32_t* O, int64_t NS, int32_t T, int32_t B,
+                              int32_t E, float* dW, int32_t* status, hipStream_t st);
+hipError_t launch_atomic_update(const TableDesc& d, const float* src, bool fused,
+                                const int32_t* I, const int32_t* O, int64_t NS, int32_t B,
+                                float lr, int32_t* status, hipStream_t st);
+hipError_t launch_owner_update(const TableDesc& d, const float* dW, const int32_t* I,
+                               const int32_t* O, int64_t NS, int32_t B, int32_t owners, float lr,
+                               hipStream_t st);
+
 hipError_t launch_split(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t st);
 hipError_t launch_combine(const uint16_t* hi, const uint16_t* lo, float* w, int64_t n,
                           hipStream_t st);

@@ -1,0 +1,74 @@
+"""The paper's unfused update designs on the GPU (measured baselines):
+Algorithm 2 (materialised dW), Algorithm 3 with FP32 atomics, the fused
+atomic update, and Algorithm 4's row-range ownership."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2005_04680_amd as pk
+from embbag_data import random_bags
+from gpu_util import DEV, GpuTables, assert_close, bits_equal, log, require_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _case(seed, rows=(2000, 37, 900), dim=64, batch=300, maxp=10, hot=0.0):
+    rng = np.random.default_rng(seed)
+    W = [rng.uniform(-0.05, 0.05, (m, dim)).astype(np.float32) for m in rows]
+    I, O = random_bags(rng, rows, batch, maxp, 0.1, hot)
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    return W, I, O, G, batch, dim
+
+
+@pytest.mark.parametrize("dim", [16, 64, 256])
+def test_materialize_is_a_copy(dim):
+    W, I, O, G, B, E = _case(1, dim=dim)
+    T = len(W)
+    dW = torch.empty((I.size, E), dtype=torch.float32, device=DEV)
+    assert pk.embbag_baseline_materialize(to_dev(G), T, B, E, to_dev(O), I.size, dW) == 0
+    bag = np.searchsorted(O, np.arange(I.size), side="right") - 1
+    assert bits_equal(dW.cpu().numpy(), G.reshape(-1, E)[bag])
+
+
+@pytest.mark.parametrize("owners", [1, 7, 256])
+@pytest.mark.parametrize("dim", [16, 256, 1024])
+def test_owner_update_equals_sequential_fp32(owners, dim):
+    """Algorithm 4 applies each row's look-ups in increasing s in FP32: bit for
+    bit the oracle's literal reading of Algorithms 2 and 3."""
+    W, I, O, G, B, E = _case(2 + owners, dim=dim, hot=0.3)
+    T = len(W)
+    log(f"[owner] owners={owners} dim={dim} NS={I.size}")
+    gt = GpuTables(W)
+    dW = torch.empty((I.size, E), dtype=torch.float32, device=DEV)
+    assert pk.embbag_baseline_materialize(to_dev(G), T, B, E, to_dev(O), I.size, dW) == 0
+    assert pk.embbag_baseline_update_owner(dW, B, to_dev(I), to_dev(O), 0.1, gt.w, owners) == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd(G, B, I, O, 0.1, Wref, literal=True) == 0
+    for a, b in zip(gt.host(), Wref):
+        assert bits_equal(a, b)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_atomic_update_within_tolerance(fused):
+    W, I, O, G, B, E = _case(3)
+    T = len(W)
+    gt = GpuTables(W)
+    if fused:
+        assert pk.embbag_baseline_backward_sgd_atomic(to_dev(G), B, to_dev(I), to_dev(O), 0.1,
+                                                      gt.w, gt.status) == 0
+    else:
+        dW = torch.empty((I.size, E), dtype=torch.float32, device=DEV)
+        assert pk.embbag_baseline_materialize(to_dev(G), T, B, E, to_dev(O), I.size, dW) == 0
+        assert pk.embbag_baseline_update_atomic(dW, B, to_dev(I), to_dev(O), 0.1, gt.w,
+                                                gt.status) == 0
+    assert gt.read_status() == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd(G, B, I, O, 0.1, Wref) == 0
+    for t, (a, b) in enumerate(zip(gt.host(), Wref)):
+        assert_close(a, b, f"atomic table {t}")
