@@ -34,49 +34,58 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def describe(cfg):
-    if cfg.name == "mlperf":
-        return (f"mlperf: 26 tables, log-uniform rows in [10, 4e7] ({cfg.table_bytes / 1e9:.1f} GB FP32), "
-                f"E=128, batch 65536, 1 look-up/bag, Zipf(1.2)")
+def describe(cfg, act_bf16=False):
     kind = "split-BF16 hi/lo" if cfg.split else "FP32"
+    act = ", BF16 pooled outputs and gradients" if act_bf16 else ""
+    if cfg.name.startswith("mlperf"):
+        return (f"{cfg.name}: 26 tables, log-uniform rows in [10, 4e7], {kind} "
+                f"({cfg.table_bytes / 1e9:.1f} GB), E=128, batch 65536, 1 look-up/bag, "
+                f"Zipf(1.2){act}")
     dist = f"Zipf({cfg.zipf_s})" if cfg.dist == "zipf" else "uniform"
     return (f"{cfg.name}: {cfg.num_tables} tables x {cfg.rows[0]:.0e} rows x E={cfg.dim} {kind} "
-            f"({cfg.table_bytes / 1e9:.1f} GB), batch {cfg.batch}, {cfg.pooling} look-ups/bag, {dist}")
+            f"({cfg.table_bytes / 1e9:.1f} GB), batch {cfg.batch}, {cfg.pooling} look-ups/bag, "
+            f"{dist}{act}")
 
 
-def bytes_model(cfg, U, split):
-    """Algorithmic HBM bytes of one step (forward, backward+update)."""
+def bytes_model(cfg, U, split, act_bf16=False):
+    """Algorithmic HBM bytes of one step (forward, backward+update).  Row reads of
+    the forward are s_w = 4 B (FP32) or 2 B (BF16 hi halves) per element; pooled
+    outputs and their gradients s_y = 4 B or 2 B (BF16 activations); the update
+    reads and writes 4 B per element of every touched row (FP32, or hi + lo)."""
     T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
     TB = T * B
     sw = 2 if split else 4
-    fwd = NS * E * sw + 4 * NS + 4 * (TB + 1) + 4 * TB * E
-    bwd = 4 * TB * E + 4 * NS + 4 * (TB + 1) + 2 * U * E * 4
+    sy = 2 if act_bf16 else 4
+    fwd = NS * E * sw + 4 * NS + 4 * (TB + 1) + sy * TB * E
+    bwd = sy * TB * E + 4 * NS + 4 * (TB + 1) + 2 * U * E * 4
     return fwd, bwd
 
 
-def profiled_traffic(cfg, kernels):
-    """HBM-side bytes per launch of `kernels` from profiles/traffic.json (copy-calibrated
-    rocprofv3 FETCH_SIZE + WRITE_SIZE), or None when that record is for another
-    workload or the kernels' sources changed since the counters were taken."""
+def profiled_traffic(workload, call):
+    """HBM-side bytes per launch of one call ("forward" or "apply", all its
+    kernels) from profiles/traffic.json (copy-calibrated rocprofv3 FETCH_SIZE +
+    WRITE_SIZE), or None when that record is for another workload or the
+    kernels' sources changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("workload") != cfg.name:
+    if rec.get("workload") != workload:
         return None
-    total = 0
-    for k in kernels:
-        r = rec["kernels"].get(k)
-        if r is None:
-            return None
-        h = hashlib.sha256()
-        for src in r["sources"]:
-            h.update(open(os.path.join(ROOT, src), "rb").read())
-        if h.hexdigest() != r["source_sha256"]:
-            return None
-        total += r["fetch_bytes"] + r["write_bytes"]
-    return total
+    r = rec.get("calls", {}).get(call)
+    if r is None:
+        return None
+    h = hashlib.sha256()
+    for src in r["sources"]:
+        h.update(open(os.path.join(ROOT, src), "rb").read())
+    if h.hexdigest() != r["source_sha256"]:
+        return None
+    return r["fetch_bytes"] + r["write_bytes"]
+
+
+def workload_tag(cfg, act_bf16):
+    return cfg.name + ("+bf16act" if act_bf16 else "")
 
 
 def unique_count(cfg, I):
@@ -85,7 +94,7 @@ def unique_count(cfg, I):
     return int(sum(np.unique(I[t * n_t:(t + 1) * n_t]).size for t in range(cfg.num_tables)))
 
 
-def cpu_baseline(cfg, batch_I, G, sample_bags):
+def cpu_baseline(cfg, batch_I, G, sample_bags, act_bf16=False):
     """The CPU oracle on the first `sample_bags` bags of every table of batch 0."""
     import torch
 
@@ -105,7 +114,15 @@ def cpu_baseline(cfg, batch_I, G, sample_bags):
     I_s = np.concatenate(I_s)
     O_s = np.arange(0, T * nb * P + 1, P, dtype=np.int32)
     G_s = np.ascontiguousarray(G[:, :nb, :])
-    if cfg.split:
+    if cfg.split and act_bf16:
+        his, los = zip(*[oracle.split(w) for w in tabs])
+        his, los = list(his), list(los)
+        Gb = np.ascontiguousarray(torch.from_numpy(G_s).to(torch.bfloat16).view(torch.int16)
+                                  .numpy().view(np.uint16))
+        t0 = time.perf_counter()
+        rc1, _ = oracle.forward_split_bf16_act(his, nb, I_s, O_s)
+        rc2 = oracle.backward_sgd_split_bf16_act(Gb, nb, I_s, O_s, cfg.lr, his, los)
+    elif cfg.split:
         his, los = zip(*[oracle.split(w) for w in tabs])
         his, los = list(his), list(los)
         t0 = time.perf_counter()
@@ -163,8 +180,11 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="large",
-                    choices=["tiny", "small", "large", "mlperf", "split", "small_p50_uniform",
-                             "large_uniform"])
+                    choices=["tiny", "small", "large", "mlperf", "split", "large_split",
+                             "mlperf_split", "small_p50_uniform", "large_uniform"])
+    ap.add_argument("--act", default="f32", choices=["f32", "bf16"],
+                    help="pooled outputs and their gradients in FP32, or in BF16 (split-storage "
+                         "configurations only: Section VII's BF16 activations)")
     ap.add_argument("--batches", type=int, default=4, help="pre-generated batches, rotated")
     ap.add_argument("--cpu-sample-bags", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -209,6 +229,10 @@ def main():
     cfg = get_config(args.config)
     T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
     split = cfg.split
+    act_bf16 = args.act == "bf16"
+    if act_bf16 and not split:
+        print(json.dumps({"error": "--act bf16 needs a split-storage configuration"}))
+        sys.exit(2)
 
     # ---- tables in HBM ----------------------------------------------------
     t0 = time.time()
@@ -234,17 +258,22 @@ def main():
         I, O = make_batch(cfg, b, device=dev)
         G = make_grads(cfg, b)
         U = unique_count(cfg, I)
+        Gd = torch.from_numpy(G).to(dev)
+        if act_bf16:
+            Gd = Gd.to(torch.bfloat16)  # the gradient a BF16 network hands over
         batches.append(dict(I=torch.from_numpy(I).to(dev), O=torch.from_numpy(O).to(dev),
-                            G=torch.from_numpy(G).to(dev), U=U, I_host=I if b == 0 else None,
+                            G=Gd, U=U, I_host=I if b == 0 else None,
                             G_host=G if b == 0 else None))
     log(f"[bench] {args.batches} batches generated in {time.time() - t0:.1f}s; "
         f"U = {[x['U'] for x in batches]}")
 
-    Y = torch.empty((T, B, E), dtype=torch.float32, device=dev)
+    Y = torch.empty((T, B, E), dtype=torch.bfloat16 if act_bf16 else torch.float32, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8, device=dev)
 
     def fwd(bt):
+        if act_bf16:
+            return pk.embbag_forward_split_bf16_act(hi, B, bt["I"], bt["O"], Y, status)
         if split:
             return pk.embbag_forward_split_bf16(hi, B, bt["I"], bt["O"], Y, status)
         return pk.embbag_forward(tables, B, bt["I"], bt["O"], Y, status)
@@ -253,6 +282,8 @@ def main():
         return pk.embbag_backward_prepare(cfg.rows, E, B, bt["I"], bt["O"], ws, status)
 
     def apply(bt):
+        if act_bf16:
+            return pk.embbag_backward_apply_sgd_split_bf16_act(bt["G"], B, NS, cfg.lr, hi, lo, ws)
         if split:
             return pk.embbag_backward_apply_sgd_split_bf16(bt["G"], B, NS, cfg.lr, hi, lo, ws)
         return pk.embbag_backward_apply_sgd(bt["G"], B, NS, cfg.lr, tables, ws)
@@ -308,30 +339,27 @@ def main():
     apply_ms = sum(e[4].elapsed_time(e[5]) for e in ev) / K
     ms_step = total_ms / K
     U_avg = sum(batches[i % len(batches)]["U"] for i in range(K)) / K
-    fwd_b, bwd_b = bytes_model(cfg, U_avg, split)
+    fwd_b, bwd_b = bytes_model(cfg, U_avg, split, act_bf16)
     step_b = fwd_b + bwd_b
     gbps = step_b / (ms_step * 1e-3) / 1e9
     # Roofline of the dominant kernel.  The forward call is one launch
     # (fwd_gather_sum); the apply call is segment_sgd plus the short
     # segment_fixup, whose events bracket both.  Algorithmic bytes per launch:
-    # forward = NS*E*s_w + 4*NS + 4*(TB+1) + 4*TB*E (every look-up reads its
-    # row); apply = dY once (4*TB*E) + the sorted look-ups (8*NS) + one read and
-    # one write of every touched row (2*U*E*s_row).
+    # forward = NS*E*s_w + 4*NS + 4*(TB+1) + s_y*TB*E (every look-up reads its
+    # row); apply = dY once (s_y*TB*E) + the sorted look-ups (8*NS) + one read
+    # and one write of every touched row (2*U*E*4).
     TB = T * B
-    apply_b = 4 * TB * E + 8 * NS + 2 * U_avg * E * 4
-    lpr = 64 if E >= 256 else max(1, 1 << max(0, (E // 4 - 1).bit_length()))
-    cpl = max(1, E // 4 // 64)
-    rows_t = "SplitRows" if split else "Fp32Rows"
+    sy = 2 if act_bf16 else 4
+    apply_b = sy * TB * E + 8 * NS + 2 * U_avg * E * 4
     if apply_ms >= fwd_ms:
-        roof_k, roof_b, roof_ms = "segment_sgd+segment_fixup", apply_b, apply_ms
-        kern = [f"segment_sgd<{lpr}, {cpl}, {rows_t}>", f"segment_fixup<{lpr}, {cpl}, {rows_t}>"]
+        roof_call, roof_k, roof_b, roof_ms = "apply", "segment_sgd+segment_fixup", apply_b, apply_ms
     else:
-        roof_k, roof_b, roof_ms = "fwd_gather_sum", fwd_b, fwd_ms
-        kern = [f"fwd_gather_sum<{lpr}, {cpl}, {'true' if split else 'false'}>"]
+        roof_call, roof_k, roof_b, roof_ms = "forward", "fwd_gather_sum", fwd_b, fwd_ms
     achieved = roof_b / (roof_ms * 1e-3) / 1e9
     roof = {"kernel": roof_k, "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": profiled_traffic(cfg, kern), "bytes_per_launch": int(roof_b),
+            "traffic": profiled_traffic(workload_tag(cfg, act_bf16), roof_call),
+            "bytes_per_launch": int(roof_b),
             "avg_launch_ms": round(roof_ms, 4)}
 
     out = {
@@ -347,7 +375,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": describe(cfg), "tables": T, "dim": E, "batch": B,
+        "config": {"workload": describe(cfg, act_bf16), "tables": T, "dim": E, "batch": B,
                    "pooling": cfg.pooling, "num_indices": NS, "unique_rows": round(U_avg),
                    "lr": cfg.lr, "batches_rotated": args.batches,
                    "streams": 2 if args.overlap_prepare else 1},
@@ -364,7 +392,8 @@ def main():
         out["baselines"] = time_baselines(pk, torch, cfg, tables, batches, main)
     if not args.no_cpu_baseline:
         b0 = batches[0]
-        out["cpu_baseline"] = cpu_baseline(cfg, b0["I_host"], b0["G_host"], args.cpu_sample_bags)
+        out["cpu_baseline"] = cpu_baseline(cfg, b0["I_host"], b0["G_host"], args.cpu_sample_bags,
+                                           act_bf16)
     print(json.dumps(out), flush=True)
 
 

@@ -13,7 +13,8 @@ The graded single-GPU variants differ from the paper where noted:
 * ``mlperf`` : 26 tables, E=128, rows log-uniform in [10, 4e7] conditioned so
                that all tables together take ~98 GB (Table 2), batch 65536,
                P=1, Zipf(1.2).
-* ``split``  : ``small`` stored as Split-SGD-BF16 halves (Section VII).
+* ``split``  : ``small`` stored as Split-SGD-BF16 halves (Section VII);
+  ``large_split`` and ``mlperf_split`` are the same storage at those shapes.
 * ``tiny``   : 4 x 1000 x 16, batch 32, P=4, uniform; values U(-0.01, 0.01).
 
 Table values are U(-a_t, a_t) with a_t = 1/sqrt(M_t) (0.01 for ``tiny``);
@@ -89,6 +90,10 @@ def _make(name: str, seed: int) -> Config:
         rows, _attempt = mlperf_rows(seed)
         rows = tuple(int(r) for r in rows)
         return Config("mlperf", rows, 128, 65536, 1, "zipf", 1.2, _uniform_scale(rows), seed=seed)
+    if name == "large_split":
+        return _make("large", seed).with_(name=name, split=True)
+    if name == "mlperf_split":
+        return _make("mlperf", seed).with_(name=name, split=True)
     if name == "small_p50_uniform":
         rows = (1_000_000,) * 8
         return Config(name, rows, 64, 2048, 50, "uniform", 0.0, _uniform_scale(rows), seed=seed)
@@ -97,7 +102,7 @@ def _make(name: str, seed: int) -> Config:
     raise KeyError(f"unknown config {name!r}; known: {CONFIG_NAMES}")
 
 
-CONFIG_NAMES = ("tiny", "small", "large", "mlperf", "split",
+CONFIG_NAMES = ("tiny", "small", "large", "mlperf", "split", "large_split", "mlperf_split",
                 "small_p50_uniform", "large_uniform")
 
 _CACHE: dict = {}

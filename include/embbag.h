@@ -188,6 +188,32 @@ int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
                                    size_t workspace_bytes, int32_t* d_status,
                                    hipStream_t stream);
 
+/* BF16 activations (Section VII trains with BF16 activations and gradients
+ * and keeps the FP32 weight only for the update).  Same operations as the
+ * split entry points above, with the pooled output and its gradient stored as
+ * BF16 bit patterns, [T][B][E] uint16, 8-byte aligned:
+ *   - forward: each pooled value is the FP32 sum of the bag's high halves
+ *     (as embbag_forward_split_bf16), rounded to the nearest BF16, ties to
+ *     even; an empty bag gives +0;
+ *   - backward: each gradient value is widened exactly (g << 16 as FP32) and
+ *     the update is that of embbag_backward_sgd_split_bf16.
+ * Errors, workspace and phases as for the FP32-activation entry points. */
+int embbag_forward_split_bf16_act(const embbag_split_tables_t* tables, int32_t batch,
+                                  const int32_t* indices, const int32_t* offsets,
+                                  int64_t num_indices, uint16_t* pooled_out, int32_t* d_status,
+                                  hipStream_t stream);
+int embbag_backward_sgd_split_bf16_act(const uint16_t* grad_pooled, int32_t batch,
+                                       const int32_t* indices, const int32_t* offsets,
+                                       int64_t num_indices, float lr,
+                                       const embbag_split_tables_t* tables, void* workspace,
+                                       size_t workspace_bytes, int32_t* d_status,
+                                       hipStream_t stream);
+int embbag_backward_apply_sgd_split_bf16_act(const uint16_t* grad_pooled, int32_t batch,
+                                             int64_t num_indices, float lr,
+                                             const embbag_split_tables_t* tables,
+                                             void* workspace, size_t workspace_bytes,
+                                             hipStream_t stream);
+
 /* Section VII storage helpers (device, elementwise over n values):
  * hi[i] = bits(w[i]) >> 16, lo[i] = bits(w[i]) & 0xFFFF, and the inverse
  * w[i] = from_bits(hi[i] << 16 | lo[i]).  Lossless in both directions. */

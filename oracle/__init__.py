@@ -49,6 +49,10 @@ def lib():
         L.oracle_backward_sgd_split.argtypes = [p, i32, i32, i32, p, p, p, p, p, i64, f32]
         L.oracle_forward_weighted.argtypes = [i32, i32, i32, p, p, p, p, i64, p, i32, p]
         L.oracle_backward_sgd_weighted.argtypes = [p, i32, i32, i32, p, p, p, p, i64, p, i32, f32]
+        L.oracle_bf16_round.argtypes = [p, p, i64]
+        L.oracle_bf16_widen.argtypes = [p, p, i64]
+        L.oracle_forward_split_bf16_act.argtypes = [i32, i32, i32, p, p, p, p, i64, p]
+        L.oracle_backward_sgd_split_bf16_act.argtypes = [p, i32, i32, i32, p, p, p, p, p, i64, f32]
         L.oracle_split.argtypes = [p, p, p, i64]
         L.oracle_combine.argtypes = [p, p, p, i64]
         L.oracle_split_roundtrip_mismatches.argtypes = [C.c_uint64, C.c_uint64]
@@ -56,7 +60,8 @@ def lib():
         for name in ("oracle_validate", "oracle_forward", "oracle_forward_literal",
                      "oracle_forward_split", "oracle_dedup", "oracle_backward_sgd",
                      "oracle_backward_sgd_literal", "oracle_backward_sgd_split",
-                     "oracle_forward_weighted", "oracle_backward_sgd_weighted"):
+                     "oracle_forward_weighted", "oracle_backward_sgd_weighted",
+                     "oracle_forward_split_bf16_act", "oracle_backward_sgd_split_bf16_act"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -187,6 +192,48 @@ def backward_sgd_weighted(grad, batch: int, indices, offsets, lr: float, tables,
     rows = _rows(tables)
     return lib().oracle_backward_sgd_weighted(_ptr(G), T, batch, E, _ptr(rows), _ptr_array(tables),
                                               _ptr(I), _ptr(O), I.size, _ptr(a), mode, lr)
+
+
+def bf16_round(x):
+    """FP32 -> BF16 bit patterns (uint16), round to nearest, ties to even."""
+    x = _c(x, np.float32)
+    out = np.empty(x.shape, np.uint16)
+    lib().oracle_bf16_round(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+def bf16_widen(h):
+    """BF16 bit patterns (uint16) -> FP32, exact."""
+    h = _c(h, np.uint16)
+    out = np.empty(h.shape, np.float32)
+    lib().oracle_bf16_widen(_ptr(h), _ptr(out), h.size)
+    return out
+
+
+def forward_split_bf16_act(hi_tables, batch: int, indices, offsets):
+    """Split forward with BF16 pooled outputs.  Returns (status, pooled uint16 [T, B, E])."""
+    hi_tables = [_c(t, np.uint16) for t in hi_tables]
+    I, O = _c(indices, np.int32), _c(offsets, np.int32)
+    T, E = len(hi_tables), hi_tables[0].shape[1]
+    rows = _rows(hi_tables)
+    Y = np.zeros((T, batch, E), dtype=np.uint16)
+    rc = lib().oracle_forward_split_bf16_act(T, batch, E, _ptr(rows), _ptr_array(hi_tables),
+                                             _ptr(I), _ptr(O), I.size, _ptr(Y))
+    return rc, Y
+
+
+def backward_sgd_split_bf16_act(grad_bf16, batch: int, indices, offsets, lr: float, hi_tables,
+                                lo_tables) -> int:
+    """Split update driven by a BF16 gradient (uint16 bit patterns [T, B, E])."""
+    hi_tables = [_c(t, np.uint16) for t in hi_tables]
+    lo_tables = [_c(t, np.uint16) for t in lo_tables]
+    G = _c(grad_bf16, np.uint16)
+    I, O = _c(indices, np.int32), _c(offsets, np.int32)
+    T, E = len(hi_tables), hi_tables[0].shape[1]
+    rows = _rows(hi_tables)
+    return lib().oracle_backward_sgd_split_bf16_act(_ptr(G), T, batch, E, _ptr(rows),
+                                                    _ptr_array(hi_tables), _ptr_array(lo_tables),
+                                                    _ptr(I), _ptr(O), I.size, lr)
 
 
 def split(w):

@@ -28,6 +28,7 @@
 // Build: g++ -O2 -std=c++17 -fno-fast-math -ffp-contract=off -shared -fPIC
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 #include <numeric>
@@ -303,6 +304,82 @@ int oracle_backward_sgd_split(const float* dY, int32_t T, int32_t B, int32_t E,
       oracle_split(&w, h + e, l + e, 1);
     }
   });
+}
+
+// ---- BF16 activations.  Section VII runs the forward and backward passes in
+// ---- BF16 and keeps FP32 only for the weight update; a BF16 number is an
+// ---- FP32 value whose 16 low bits are zero.
+
+// FP32 -> BF16 by round to nearest, ties to even, from its definition: of the
+// two BF16 neighbours of x (x truncated toward zero, and the next BF16 away
+// from zero) take the nearer; on a tie the one whose last bit is 0.  Past the
+// largest finite BF16 the upper neighbour is infinity, placed at 2^128 for the
+// comparison (the value the next binade would start at), as IEEE 754 rounding
+// does.  NaN stays NaN (quiet).
+void oracle_bf16_round(const float* x, uint16_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) {
+    const float f = x[i];
+    const uint32_t u = float_to_bits(f);
+    if (std::isnan(f)) {
+      out[i] = uint16_t((u >> 16) | 0x40u);
+      continue;
+    }
+    const uint32_t down = u & 0xFFFF0000u;
+    if (down == u) {  // already a BF16 number (zeros and infinities included)
+      out[i] = uint16_t(down >> 16);
+      continue;
+    }
+    const uint32_t up = down + 0x10000u;  // next in magnitude, same sign
+    const double vd = double(bits_to_float(down));
+    const double vu = (up & 0x7FFFFFFFu) == 0x7F800000u ? std::copysign(std::ldexp(1.0, 128), f)
+                                                         : double(bits_to_float(up));
+    const double dd = std::fabs(double(f) - vd), du = std::fabs(vu - double(f));
+    uint32_t pick;
+    if (dd < du)
+      pick = down;
+    else if (du < dd)
+      pick = up;
+    else
+      pick = ((down >> 16) & 1u) == 0 ? down : up;
+    out[i] = uint16_t(pick >> 16);
+  }
+}
+
+// BF16 -> FP32 is exact: the 16 bits become the high half.
+void oracle_bf16_widen(const uint16_t* h, float* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = bits_to_float(uint32_t(h[i]) << 16);
+}
+
+// Forward of Section VII with BF16 pooled outputs: the FP32 pooled sums of
+// oracle_forward_split, each rounded to BF16.
+int oracle_forward_split_bf16_act(int32_t T, int32_t B, int32_t E, const int64_t* rows,
+                                  const uint16_t* const* hi, const int32_t* I, const int32_t* O,
+                                  int64_t NS, uint16_t* Y) {
+  if (hi == nullptr || Y == nullptr) return kErrInvalidArg;
+  int rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
+  std::vector<float> y(size_t(T) * size_t(B) * size_t(E), 0.0f);
+  rc = oracle_forward_split(T, B, E, rows, hi, I, O, NS, y.data());
+  if (rc) return rc;
+  oracle_bf16_round(y.data(), Y, int64_t(y.size()));
+  return kOk;
+}
+
+// Update of Section VII driven by a BF16 gradient of the pooled output: the
+// gradient is widened to FP32, then oracle_backward_sgd_split applies.
+int oracle_backward_sgd_split_bf16_act(const uint16_t* dY, int32_t T, int32_t B, int32_t E,
+                                       const int64_t* rows, uint16_t* const* hi,
+                                       uint16_t* const* lo, const int32_t* I, const int32_t* O,
+                                       int64_t NS, float lr) {
+  if (hi == nullptr || lo == nullptr) return kErrInvalidArg;
+  const int rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
+  if (dY == nullptr && NS > 0) return kErrInvalidArg;
+  const int64_t n = int64_t(T) * B * E;
+  std::vector<float> g(static_cast<size_t>(n));
+  if (n > 0 && dY != nullptr) oracle_bf16_widen(dY, g.data(), n);
+  return oracle_backward_sgd_split(dY != nullptr ? g.data() : nullptr, T, B, E, rows, hi, lo, I,
+                                   O, NS, lr);
 }
 
 // ---- Literal readings, kept only to show how far FP32 sequential order

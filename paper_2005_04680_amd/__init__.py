@@ -71,6 +71,10 @@ def lib():
         L.embbag_backward_prepare.argtypes = [i32, p, i32, i32, p, p, i64, p, sz, p, p]
         L.embbag_backward_apply_sgd.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
         L.embbag_backward_apply_sgd_split_bf16.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
+        L.embbag_forward_split_bf16_act.argtypes = [p, i32, p, p, i64, p, p, p]
+        L.embbag_backward_sgd_split_bf16_act.argtypes = [p, i32, p, p, i64, C.c_float, p, p, sz,
+                                                         p, p]
+        L.embbag_backward_apply_sgd_split_bf16_act.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
         L.embbag_split_fp32.argtypes = [p, p, p, i64, p]
         L.embbag_combine_fp32.argtypes = [p, p, p, i64, p]
         L.embbag_dedup_workspace_bytes.argtypes = [i32, i32, i64]
@@ -85,6 +89,8 @@ def lib():
                   "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
                   "embbag_forward_pooled", "embbag_backward_sgd_pooled",
                   "embbag_backward_apply_sgd", "embbag_backward_apply_sgd_split_bf16",
+                  "embbag_forward_split_bf16_act", "embbag_backward_sgd_split_bf16_act",
+                  "embbag_backward_apply_sgd_split_bf16_act",
                   "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
                   "embbag_baseline_materialize", "embbag_baseline_update_atomic",
                   "embbag_baseline_backward_sgd_atomic", "embbag_baseline_update_owner",
@@ -265,6 +271,43 @@ def embbag_backward_apply_sgd_split_bf16(grad_pooled, batch, num_indices, lr, hi
     s, keep = _tables_struct(hi, split_lo=lo)
     return lib().embbag_backward_apply_sgd_split_bf16(
         _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch), int(num_indices), float(lr),
+        C.byref(s), _ptr(workspace, None, "workspace"),
+        int(workspace.numel() * workspace.element_size()), _stream(stream))
+
+
+# BF16 activations: pooled outputs and their gradients as torch.bfloat16 (or
+# 16-bit integer tensors holding BF16 bit patterns).
+_BF16 = ("bfloat16",) + _U16
+
+
+def embbag_forward_split_bf16_act(hi, batch, indices, offsets, pooled_out, d_status=None,
+                                  stream=None) -> int:
+    s, keep = _split_struct_fwd(hi)
+    return lib().embbag_forward_split_bf16_act(C.byref(s), int(batch),
+                                               _ptr(indices, _dt(*_I32), "indices"),
+                                               _ptr(offsets, _dt(*_I32), "offsets"),
+                                               int(indices.numel()),
+                                               _ptr(pooled_out, _dt(*_BF16), "pooled_out"),
+                                               _ptr(d_status, _dt(*_I32), "d_status"),
+                                               _stream(stream))
+
+
+def embbag_backward_sgd_split_bf16_act(grad_pooled, batch, indices, offsets, lr, hi, lo,
+                                       workspace, d_status=None, stream=None) -> int:
+    s, keep = _tables_struct(hi, split_lo=lo)
+    return lib().embbag_backward_sgd_split_bf16_act(
+        _ptr(grad_pooled, _dt(*_BF16), "grad_pooled"), int(batch),
+        _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
+        int(indices.numel()), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
+        int(workspace.numel() * workspace.element_size()),
+        _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_apply_sgd_split_bf16_act(grad_pooled, batch, num_indices, lr, hi, lo,
+                                             workspace, stream=None) -> int:
+    s, keep = _tables_struct(hi, split_lo=lo)
+    return lib().embbag_backward_apply_sgd_split_bf16_act(
+        _ptr(grad_pooled, _dt(*_BF16), "grad_pooled"), int(batch), int(num_indices), float(lr),
         C.byref(s), _ptr(workspace, None, "workspace"),
         int(workspace.numel() * workspace.element_size()), _stream(stream))
 

@@ -63,14 +63,16 @@ int pool_mode(const float* weights, int32_t pooling) {
   return -1;
 }
 
+// Pooled outputs and their gradients: FP32 (16-B aligned rows of float4) or
+// BF16 bit patterns (8-B aligned).
 int forward_common(const TableDesc& d, bool split, int32_t B, const int32_t* I, const int32_t* O,
-                   int64_t NS, float* Y, int32_t* d_status, const PoolArgs& pool,
+                   int64_t NS, void* Y, bool y_bf16, int32_t* d_status, const PoolArgs& pool,
                    hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
-  if (int64_t(d.num_tables) * B > 0 && (Y == nullptr || !aligned(Y, 16)))
+  if (int64_t(d.num_tables) * B > 0 && (Y == nullptr || !aligned(Y, y_bf16 ? 8 : 16)))
     return EMBBAG_ERR_INVALID_ARG;
-  return hip_status(launch_forward(d, split, B, I, O, NS, Y, d_status, pool, st));
+  return hip_status(launch_forward(d, split, B, I, O, NS, Y, y_bf16, d_status, pool, st));
 }
 
 int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O, int64_t NS,
@@ -85,30 +87,39 @@ int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_
                                 mode == kPoolWeighted, st));
 }
 
-int apply_common(const TableDesc& d, bool split, const float* dY, int32_t B, int64_t NS, float lr,
-                 void* ws, size_t ws_bytes, const PoolArgs& pool, hipStream_t st) {
+int apply_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16, int32_t B,
+                 int64_t NS, float lr, void* ws, size_t ws_bytes, const PoolArgs& pool,
+                 hipStream_t st) {
   if (B < 0 || NS < 0 || NS > kInt32Max || int64_t(d.num_tables) * B + 1 > kInt32Max)
     return EMBBAG_ERR_INVALID_ARG;
   if (int64_t(d.num_tables) * B == 0 && NS > 0) return EMBBAG_ERR_OFFSETS;
-  if (NS > 0 && (dY == nullptr || !aligned(dY, 16))) return EMBBAG_ERR_INVALID_ARG;
+  if (NS > 0 && (dY == nullptr || !aligned(dY, dy_bf16 ? 8 : 16))) return EMBBAG_ERR_INVALID_ARG;
   const uint32_t total = d.rowbase[d.num_tables];
   const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
   if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
-  return hip_status(launch_segment_sgd(d, split, B, dY, lr, L, static_cast<char*>(ws),
+  return hip_status(launch_segment_sgd(d, split, B, dY, dy_bf16, lr, L, static_cast<char*>(ws),
                                        phase_token(d.num_tables, B, NS, total, pool.mode), pool,
                                        st));
 }
 
-int backward_common(const TableDesc& d, bool split, const float* dY, int32_t B, const int32_t* I,
-                    const int32_t* O, int64_t NS, float lr, void* ws, size_t ws_bytes,
-                    int32_t* d_status, const PoolArgs& pool, hipStream_t st) {
+int backward_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16, int32_t B,
+                    const int32_t* I, const int32_t* O, int64_t NS, float lr, void* ws,
+                    size_t ws_bytes, int32_t* d_status, const PoolArgs& pool, hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
-  if (NS > 0 && (dY == nullptr || !aligned(dY, 16))) return EMBBAG_ERR_INVALID_ARG;
+  if (NS > 0 && (dY == nullptr || !aligned(dY, dy_bf16 ? 8 : 16))) return EMBBAG_ERR_INVALID_ARG;
   if (pool.mode == kPoolWeighted && NS > 0 && pool.weights == nullptr) return EMBBAG_ERR_INVALID_ARG;
   rc = prepare_common(d, B, I, O, NS, ws, ws_bytes, d_status, pool.mode, st);
   if (rc) return rc;
-  return apply_common(d, split, dY, B, NS, lr, ws, ws_bytes, pool, st);
+  return apply_common(d, split, dY, dy_bf16, B, NS, lr, ws, ws_bytes, pool, st);
+}
+
+// Split tables (hi halves, and lo halves when `need_lo`): 8-B aligned.
+int split_desc(const embbag_split_tables_t* tables, bool need_lo, TableDesc* d) {
+  if (tables == nullptr || (need_lo && tables->lo == nullptr)) return EMBBAG_ERR_INVALID_ARG;
+  return make_desc(tables->num_tables, tables->dim, tables->rows,
+                   reinterpret_cast<void* const*>(tables->hi),
+                   need_lo ? reinterpret_cast<void* const*>(tables->lo) : nullptr, 8, d);
 }
 
 }  // namespace
@@ -191,8 +202,8 @@ int embbag_forward(const embbag_tables_t* tables, int32_t batch, const int32_t* 
   int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
-  return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, d_status,
-                        PoolArgs{}, stream);
+  return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, false,
+                        d_status, PoolArgs{}, stream);
 }
 
 int embbag_forward_pooled(const embbag_tables_t* tables, int32_t batch, const int32_t* indices,
@@ -210,8 +221,8 @@ int embbag_forward_pooled(const embbag_tables_t* tables, int32_t batch, const in
   pool.mode = mode;
   pool.weights = per_sample_weights;
   pool.offsets = offsets;
-  return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, d_status,
-                        pool, stream);
+  return forward_common(d, false, batch, indices, offsets, num_indices, pooled_out, false,
+                        d_status, pool, stream);
 }
 
 int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch,
@@ -223,8 +234,8 @@ int embbag_forward_split_bf16(const embbag_split_tables_t* tables, int32_t batch
   int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
                      reinterpret_cast<void* const*>(tables->hi), nullptr, 8, &d);
   if (rc) return rc;
-  return forward_common(d, true, batch, indices, offsets, num_indices, pooled_out, d_status,
-                        PoolArgs{}, stream);
+  return forward_common(d, true, batch, indices, offsets, num_indices, pooled_out, false,
+                        d_status, PoolArgs{}, stream);
 }
 
 size_t embbag_backward_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices,
@@ -245,7 +256,7 @@ int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* 
   int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
-  return backward_common(d, false, grad_pooled, batch, indices, offsets, num_indices, lr,
+  return backward_common(d, false, grad_pooled, false, batch, indices, offsets, num_indices, lr,
                          workspace, workspace_bytes, d_status, PoolArgs{}, stream);
 }
 
@@ -265,7 +276,7 @@ int embbag_backward_sgd_pooled(const float* grad_pooled, int32_t batch, const in
   pool.mode = mode;
   pool.weights = per_sample_weights;
   pool.offsets = offsets;
-  return backward_common(d, false, grad_pooled, batch, indices, offsets, num_indices, lr,
+  return backward_common(d, false, grad_pooled, false, batch, indices, offsets, num_indices, lr,
                          workspace, workspace_bytes, d_status, pool, stream);
 }
 
@@ -281,7 +292,7 @@ int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
                      reinterpret_cast<void* const*>(tables->hi),
                      reinterpret_cast<void* const*>(tables->lo), 8, &d);
   if (rc) return rc;
-  return backward_common(d, true, grad_pooled, batch, indices, offsets, num_indices, lr,
+  return backward_common(d, true, grad_pooled, false, batch, indices, offsets, num_indices, lr,
                          workspace, workspace_bytes, d_status, PoolArgs{}, stream);
 }
 
@@ -304,8 +315,8 @@ int embbag_backward_apply_sgd(const float* grad_pooled, int32_t batch, int64_t n
   int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
-  return apply_common(d, false, grad_pooled, batch, num_indices, lr, workspace, workspace_bytes,
-                      PoolArgs{}, stream);
+  return apply_common(d, false, grad_pooled, false, batch, num_indices, lr, workspace,
+                      workspace_bytes, PoolArgs{}, stream);
 }
 
 int embbag_backward_apply_sgd_split_bf16(const float* grad_pooled, int32_t batch,
@@ -318,8 +329,44 @@ int embbag_backward_apply_sgd_split_bf16(const float* grad_pooled, int32_t batch
                      reinterpret_cast<void* const*>(tables->hi),
                      reinterpret_cast<void* const*>(tables->lo), 8, &d);
   if (rc) return rc;
-  return apply_common(d, true, grad_pooled, batch, num_indices, lr, workspace, workspace_bytes,
-                      PoolArgs{}, stream);
+  return apply_common(d, true, grad_pooled, false, batch, num_indices, lr, workspace,
+                      workspace_bytes, PoolArgs{}, stream);
+}
+
+int embbag_forward_split_bf16_act(const embbag_split_tables_t* tables, int32_t batch,
+                                  const int32_t* indices, const int32_t* offsets,
+                                  int64_t num_indices, uint16_t* pooled_out, int32_t* d_status,
+                                  hipStream_t stream) {
+  TableDesc d;
+  int rc = split_desc(tables, false, &d);
+  if (rc) return rc;
+  return forward_common(d, true, batch, indices, offsets, num_indices, pooled_out, true, d_status,
+                        PoolArgs{}, stream);
+}
+
+int embbag_backward_sgd_split_bf16_act(const uint16_t* grad_pooled, int32_t batch,
+                                       const int32_t* indices, const int32_t* offsets,
+                                       int64_t num_indices, float lr,
+                                       const embbag_split_tables_t* tables, void* workspace,
+                                       size_t workspace_bytes, int32_t* d_status,
+                                       hipStream_t stream) {
+  TableDesc d;
+  int rc = split_desc(tables, true, &d);
+  if (rc) return rc;
+  return backward_common(d, true, grad_pooled, true, batch, indices, offsets, num_indices, lr,
+                         workspace, workspace_bytes, d_status, PoolArgs{}, stream);
+}
+
+int embbag_backward_apply_sgd_split_bf16_act(const uint16_t* grad_pooled, int32_t batch,
+                                             int64_t num_indices, float lr,
+                                             const embbag_split_tables_t* tables,
+                                             void* workspace, size_t workspace_bytes,
+                                             hipStream_t stream) {
+  TableDesc d;
+  int rc = split_desc(tables, true, &d);
+  if (rc) return rc;
+  return apply_common(d, true, grad_pooled, true, batch, num_indices, lr, workspace,
+                      workspace_bytes, PoolArgs{}, stream);
 }
 
 int embbag_split_fp32(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t stream) {

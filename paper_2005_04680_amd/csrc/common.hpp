@@ -118,8 +118,9 @@ inline uint64_t* sorted_buffer(const BwdLayout& L, char* ws) {
   return reinterpret_cast<uint64_t*>(ws + (passes % 2 == 0 ? L.off_a : L.off_b));
 }
 
+// Y is FP32 [T*B][E], or (y_bf16, split tables only) BF16 bit patterns.
 hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
-                          const int32_t* O, int64_t NS, float* Y, int32_t* status,
+                          const int32_t* O, int64_t NS, void* Y, bool y_bf16, int32_t* status,
                           const PoolArgs& pool, hipStream_t st);
 
 // Builds keys, validates, sorts into sorted_buffer(L, ws); stamps `token`.
@@ -129,9 +130,10 @@ hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const in
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
                        uint32_t token, bool by_lookup, hipStream_t st);
 
-hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
-                              float lr, const BwdLayout& L, char* ws, uint32_t token,
-                              const PoolArgs& pool, hipStream_t st);
+// dY is FP32 [T*B][E], or (dy_bf16, split tables only) BF16 bit patterns.
+hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const void* dY,
+                              bool dy_bf16, float lr, const BwdLayout& L, char* ws,
+                              uint32_t token, const PoolArgs& pool, hipStream_t st);
 
 hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
                          uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,

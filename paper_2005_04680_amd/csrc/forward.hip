@@ -31,10 +31,17 @@ __device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, int E, i
   }
 }
 
-template <int LPR, int CPL, bool SPLIT, bool MULTI, int MODE>
+// FP32 -> BF16, round to nearest, ties to even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t b = __float_as_uint(f);
+  if ((b & 0x7FFFFFFFu) > 0x7F800000u) return (b >> 16) | 0x40u;
+  return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+template <int LPR, int CPL, bool SPLIT, bool MULTI, int MODE, bool YBF16>
 __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
-    int32_t B, int32_t G, int32_t groups_per_table, int32_t items, float* __restrict__ Y,
+    int32_t B, int32_t G, int32_t groups_per_table, int32_t items, void* __restrict__ Y,
     int32_t* __restrict__ status, const float* __restrict__ A) {
   constexpr int R = kWave / LPR;
   constexpr int U = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
@@ -55,8 +62,8 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   int err = 0;
 
   // Stores bag k's pooled row; mean pooling divides by the bag's n look-ups.
+  // BF16 outputs are the FP32 sums rounded to nearest even.
   auto store_bag = [&](int k, const f4* acc, int n) {
-    float* y = Y + size_t(k) * E;
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
       const int c4 = rl + j * LPR;
@@ -64,7 +71,15 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
       if constexpr (MODE == kPoolMean) {
         if (n > 0) v = v / float(n);
       }
-      if (c4 < E4) *reinterpret_cast<f4*>(y + c4 * 4) = v;
+      if (c4 >= E4) continue;
+      if constexpr (YBF16) {
+        u2 h;
+        h.x = bf16_rne(v.x) | (bf16_rne(v.y) << 16);
+        h.y = bf16_rne(v.z) | (bf16_rne(v.w) << 16);
+        *reinterpret_cast<u2*>(static_cast<uint16_t*>(Y) + size_t(k) * E + c4 * 4) = h;
+      } else {
+        *reinterpret_cast<f4*>(static_cast<float*>(Y) + size_t(k) * E + c4 * 4) = v;
+      }
     }
   };
 
@@ -199,24 +214,24 @@ __global__ void fwd_empty_check(const int32_t* __restrict__ O, int32_t NS,
     atomicMin(status, EMBBAG_ERR_OFFSETS);
 }
 
-template <bool SPLIT, int MODE, int LPR, int CPL>
+template <bool SPLIT, int MODE, bool YBF16, int LPR, int CPL>
 void launch_one(dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I, const int32_t* O,
-                int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items, float* Y,
+                int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items, void* Y,
                 int32_t* status, const float* A) {
   if (G > 1)
-    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, true, MODE>), grid, dim3(kBlock), 0, st, d,
-                       I, O, NS, B, G, gpt, items, Y, status, A);
+    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, true, MODE, YBF16>), grid, dim3(kBlock), 0,
+                       st, d, I, O, NS, B, G, gpt, items, Y, status, A);
   else
-    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, false, MODE>), grid, dim3(kBlock), 0, st,
-                       d, I, O, NS, B, G, gpt, items, Y, status, A);
+    hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, false, MODE, YBF16>), grid, dim3(kBlock),
+                       0, st, d, I, O, NS, B, G, gpt, items, Y, status, A);
 }
 
-template <bool SPLIT, int MODE>
+template <bool SPLIT, int MODE, bool YBF16 = false>
 bool dispatch(RowGeom g, dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I,
               const int32_t* O, int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items,
-              float* Y, int32_t* status, const float* A) {
+              void* Y, int32_t* status, const float* A) {
 #define EMB_FWD(L, C) \
-  launch_one<SPLIT, MODE, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status, A)
+  launch_one<SPLIT, MODE, YBF16, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status, A)
   switch (g.lpr) {
     case 1: EMB_FWD(1, 1); return true;
     case 2: EMB_FWD(2, 1); return true;
@@ -239,7 +254,7 @@ bool dispatch(RowGeom g, dim3 grid, hipStream_t st, const TableDesc& d, const in
 }  // namespace
 
 hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
-                          const int32_t* O, int64_t NS, float* Y, int32_t* status,
+                          const int32_t* O, int64_t NS, void* Y, bool y_bf16, int32_t* status,
                           const PoolArgs& pool, hipStream_t st) {
   const int64_t TB = int64_t(d.num_tables) * B;
   if (TB == 0) {
@@ -259,7 +274,10 @@ hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32
   const dim3 grid(unsigned((items + per_block - 1) / per_block));
   const int32_t ns = int32_t(NS), it = int32_t(items);
   bool ok = false;
-  if (split)
+  if (split && y_bf16)
+    ok = dispatch<true, kPoolPlain, true>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status,
+                                          nullptr);
+  else if (split)
     ok = dispatch<true, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
   else if (pool.mode == kPoolWeighted)
     ok = dispatch<false, kPoolWeighted>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status,

@@ -19,6 +19,8 @@
 // Locality: each XCD owns one contiguous range of chunks, so the dY rows it
 // gathers at any time belong to one or two tables; the W rows, touched once,
 // are read and written with non-temporal hints so they do not evict them.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace embbag {
@@ -77,6 +79,34 @@ struct SplitRows {
   }
 };
 
+// Four gradient values of dY row `bag` as loaded (FP32, or BF16 bit patterns);
+// BF16 values are widened exactly only when summed, so that the loads of a
+// group stay in flight together.
+template <bool GBF16>
+struct Dy {
+  using Raw = typename std::conditional<GBF16, u2, f4>::type;
+  static __device__ __forceinline__ Raw load(const void* dY, uint32_t bag, int E, int c4) {
+    if constexpr (!GBF16)
+      return *reinterpret_cast<const f4*>(static_cast<const float*>(dY) + size_t(bag) * E + c4 * 4);
+    else
+      return *reinterpret_cast<const u2*>(static_cast<const uint16_t*>(dY) + size_t(bag) * E +
+                                          c4 * 4);
+  }
+  static __device__ __forceinline__ Raw zero() {
+    if constexpr (!GBF16)
+      return f4{0.f, 0.f, 0.f, 0.f};
+    else
+      return u2{0u, 0u};
+  }
+  static __device__ __forceinline__ f4 value(const Raw& r) {
+    if constexpr (!GBF16)
+      return r;
+    else
+      return f4{__uint_as_float(r.x << 16), __uint_as_float(r.x & 0xFFFF0000u),
+                __uint_as_float(r.y << 16), __uint_as_float(r.y & 0xFFFF0000u)};
+  }
+};
+
 __device__ __forceinline__ d4 widen(const f4& v) {
   return d4{double(v.x), double(v.y), double(v.z), double(v.w)};
 }
@@ -114,10 +144,10 @@ __device__ __forceinline__ double coef_at(uint64_t p, uint32_t bag, const PoolDe
   return 1.0;
 }
 
-template <int LPR, int CPL, class Rows, int MODE>
+template <int LPR, int CPL, class Rows, int MODE, bool GBF16>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
-    const float* __restrict__ dY, int32_t B, float inv_b, float lr,
+    const void* __restrict__ dY, int32_t B, float inv_b, float lr,
     double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
   // A data error, or no sort result for these sizes: no table writes.
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
@@ -176,7 +206,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     uint64_t p[U];
     uint32_t bg[U];
     bool dup[U], nseg[U];
-    f4 g[U][CPL];
+    typename Dy<GBF16>::Raw g[U][CPL];
     typename Rows::Pre wp[U][CPL];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -190,13 +220,11 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     for (int u = 0; u < U; ++u) bg[u] = s + u < hi ? bag_at<MODE>(p[u], pd) : 0u;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float* gy = dY + size_t(bg[u]) * E;
       const bool ld = s + u < hi && !dup[u];
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int c4 = rl + j * LPR;
-        g[u][j] = (ld && c4 < E4) ? *reinterpret_cast<const f4*>(gy + c4 * 4)
-                                   : f4{0.f, 0.f, 0.f, 0.f};
+        g[u][j] = (ld && c4 < E4) ? Dy<GBF16>::load(dY, bg[u], E, c4) : Dy<GBF16>::zero();
       }
       if (nseg[u]) {
         const int tu = table_of_bag(bg[u], B, inv_b);
@@ -231,7 +259,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
       if constexpr (MODE != kPoolPlain) c = coef_at<MODE>(p[u], bg[u], pd);
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
-        if (!dup[u]) glast[j] = g[u][j];
+        if (!dup[u]) glast[j] = Dy<GBF16>::value(g[u][j]);
         if constexpr (MODE == kPoolPlain)
           acc[j] += widen(glast[j]);
         else
@@ -323,13 +351,13 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   }
 }
 
-template <class Rows, int MODE>
+template <class Rows, int MODE, bool GBF16>
 bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
-                int32_t NS, int32_t C, int32_t nchunks, const float* dY, int32_t B, float inv_b,
+                int32_t NS, int32_t C, int32_t nchunks, const void* dY, int32_t B, float inv_b,
                 float lr, double* carry, const int32_t* flags, uint32_t token, PoolDev pd) {
 #define EMB_SEG(L, CC)                                                                     \
-  hipLaunchKernelGGL((segment_sgd<L, CC, Rows, MODE>), dim3(blocks), dim3(kBlock), 0, st, d, \
-                     sorted, NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token, pd)
+  hipLaunchKernelGGL((segment_sgd<L, CC, Rows, MODE, GBF16>), dim3(blocks), dim3(kBlock), 0, st, \
+                     d, sorted, NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token, pd)
   switch (g.lpr) {
     case 1: EMB_SEG(1, 1); return true;
     case 2: EMB_SEG(2, 1); return true;
@@ -375,8 +403,8 @@ bool launch_fix(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const
   return false;
 }
 
-template <class Rows, int MODE>
-bool launch_apply(const TableDesc& d, int32_t B, const float* dY, float lr, const BwdLayout& L,
+template <class Rows, int MODE, bool GBF16 = false>
+bool launch_apply(const TableDesc& d, int32_t B, const void* dY, float lr, const BwdLayout& L,
                   char* ws, uint32_t token, PoolDev pd, hipStream_t st) {
   const uint64_t* sorted = sorted_buffer(L, ws);
   double* carry = reinterpret_cast<double*>(ws + L.off_carry);
@@ -386,21 +414,23 @@ bool launch_apply(const TableDesc& d, int32_t B, const float* dY, float lr, cons
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const int blocks = int((L.nchunks + per_block - 1) / per_block);
   const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
-  return launch_seg<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, dY, B, inv_b, lr, carry,
-                                flags, token, pd) &&
+  return launch_seg<Rows, MODE, GBF16>(g, blocks, st, d, sorted, NS, C, nch, dY, B, inv_b, lr,
+                                       carry, flags, token, pd) &&
          launch_fix<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry, flags,
                                 token, pd);
 }
 
 }  // namespace
 
-hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const float* dY,
-                              float lr, const BwdLayout& L, char* ws, uint32_t token,
-                              const PoolArgs& pool, hipStream_t st) {
+hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const void* dY,
+                              bool dy_bf16, float lr, const BwdLayout& L, char* ws,
+                              uint32_t token, const PoolArgs& pool, hipStream_t st) {
   if (L.ns == 0) return hipSuccess;
   PoolDev pd{reinterpret_cast<const uint32_t*>(ws + L.off_bagof), pool.weights, pool.offsets};
   bool ok;
-  if (split)
+  if (split && dy_bf16)
+    ok = launch_apply<SplitRows, kPoolPlain, true>(d, B, dY, lr, L, ws, token, pd, st);
+  else if (split)
     ok = launch_apply<SplitRows, kPoolPlain>(d, B, dY, lr, L, ws, token, pd, st);
   else if (pool.mode == kPoolWeighted)
     ok = launch_apply<Fp32Rows, kPoolWeighted>(d, B, dY, lr, L, ws, token, pd, st);

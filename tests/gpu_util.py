@@ -42,6 +42,39 @@ def assert_close(gpu, ref, what, rtol=RTOL, atol=ATOL):
                              f"first at {i}: gpu {g[i]!r} oracle {r[i]!r}")
 
 
+def bf16_bits(t):
+    """Host uint16 bit patterns of a GPU bfloat16 (or 16-bit integer) tensor."""
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def to_bf16_bits(x):
+    """FP32 host array -> BF16 bit patterns by torch's round-to-nearest-even
+    (input preparation: the gradient an upstream BF16 network hands over)."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def assert_bf16_bracket(gpu_bits, ref32, what, rtol=RTOL, atol=ATOL):
+    """BF16 pooled outputs: the GPU rounds its FP32 sum, which is within the
+    FP32 tolerance of the oracle's, to the nearest BF16.  Rounding is monotone,
+    so each GPU value must lie between the roundings of ref -/+ tolerance.
+    Returns the number of values that differ from the rounding of ref itself."""
+    r = np.asarray(ref32, np.float64)
+    tol = atol + rtol * np.abs(r)
+    lo32 = np.nextafter((r - tol).astype(np.float32), np.float32(-np.inf))
+    hi32 = np.nextafter((r + tol).astype(np.float32), np.float32(np.inf))
+    lo = oracle.bf16_widen(oracle.bf16_round(lo32))
+    hi = oracle.bf16_widen(oracle.bf16_round(hi32))
+    g = oracle.bf16_widen(np.ascontiguousarray(gpu_bits, np.uint16))
+    bad = ~((g >= lo) & (g <= hi))
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError(f"{what}: {int(bad.sum())} BF16 values outside the rounding bracket; "
+                             f"first at {i}: gpu {g[i]!r} oracle fp32 {r[i]!r}")
+    exact = oracle.bf16_round(np.ascontiguousarray(ref32, np.float32))
+    return int((np.ascontiguousarray(gpu_bits, np.uint16) != exact).sum())
+
+
 def bits_equal(a, b):
     a = np.ascontiguousarray(a)
     b = np.ascontiguousarray(b)

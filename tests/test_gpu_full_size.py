@@ -8,7 +8,9 @@ counter-based generator, never read back from the GPU path), with indices
 remapped monotonically, so sums, sort order and segments are unchanged.
 Checked: every pooled output and every touched row (within tolerance), 10^4
 sampled untouched rows per table group (bit-identical), the full integer
-dedup (bit-exact), and the device fill against the host generator.
+dedup (bit-exact), and the device fill against the host generator.  The
+split-storage runs (Section VII) check FP32 and BF16 pooled outputs and the
+update driven by an FP32 (Large-shaped) or BF16 (MLPerf-style) gradient.
 """
 import numpy as np
 import pytest
@@ -16,9 +18,10 @@ import torch
 
 import oracle
 import paper_2005_04680_amd as pk
-from embbag_data import (fill_tables_torch, get_config, make_batch, make_grads, table_rows_torch,
-                         table_values_np)
-from gpu_util import DEV, assert_close, bits_equal, gpu_dedup, log, require_gpu
+from embbag_data import (fill_table_torch, fill_tables_torch, get_config, make_batch, make_grads,
+                         table_rows_torch, table_values_np)
+from gpu_util import (DEV, assert_bf16_bracket, assert_close, bf16_bits, bits_equal, gpu_dedup, log,
+                      require_gpu, to_bf16_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -97,9 +100,109 @@ def _run(name):
     log(f"[full] {name}: ok, U = {d['num_unique']}")
 
 
+def _run_split(name, grad_bf16):
+    """Split-SGD-BF16 storage at full size: FP32 and BF16 pooled outputs from
+    the hi halves, then the update driven by an FP32 or a BF16 gradient."""
+    cfg = get_config(name)
+    T, B, E, P, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.pooling, cfg.num_indices
+    log(f"[full] {name}: filling {cfg.table_bytes / 1e9:.1f} GB of hi/lo halves on the device")
+    hi = [torch.empty((m, E), dtype=torch.int16, device=DEV) for m in cfg.rows]
+    lo = [torch.empty((m, E), dtype=torch.int16, device=DEV) for m in cfg.rows]
+    for t, m in enumerate(cfg.rows):
+        tmp = torch.empty((m, E), dtype=torch.float32, device=DEV)
+        fill_table_torch(cfg, t, tmp)
+        assert pk.embbag_split_fp32(tmp, hi[t], lo[t]) == 0
+        del tmp
+    I, O = make_batch(cfg, 0, device=DEV)
+    G = make_grads(cfg, 0)
+    rng = np.random.default_rng(8)
+
+    # the device halves are the host generator's values, split on the host
+    for t in (0, T - 1):
+        r = np.unique(rng.integers(0, cfg.rows[t], 64))
+        h_ref, l_ref = oracle.split(table_values_np(cfg.seed, t, r, E, cfg.value_scale[t]))
+        rd = torch.from_numpy(r).to(DEV)
+        assert bits_equal(hi[t][rd].cpu().numpy().view(np.uint16), h_ref), f"hi, table {t}"
+        assert bits_equal(lo[t][rd].cpu().numpy().view(np.uint16), l_ref), f"lo, table {t}"
+
+    log(f"[full] {name}: building compact tables")
+    sel, I_c, untouched = [], np.empty_like(I), []
+    for t in range(T):
+        a, b = t * B * P, (t + 1) * B * P
+        touched = np.unique(I[a:b])
+        cand = rng.integers(0, cfg.rows[t], 2000)
+        cand = np.setdiff1d(np.unique(cand), touched)[: max(1, 10000 // T)]
+        rows = np.union1d(touched, cand)
+        I_c[a:b] = np.searchsorted(rows, I[a:b])
+        sel.append(rows)
+        untouched.append(cand)
+    hl_c = [oracle.split(table_rows_torch(cfg.seed, t, torch.from_numpy(sel[t]).to(DEV), E,
+                                          cfg.value_scale[t]).cpu().numpy()) for t in range(T)]
+    hi_c = [h for h, _ in hl_c]
+    lo_c = [l for _, l in hl_c]
+
+    log(f"[full] {name}: GPU forward (FP32 and BF16 outputs) + backward "
+        f"({'BF16' if grad_bf16 else 'FP32'} gradient)")
+    Id, Od = (torch.from_numpy(a).to(DEV) for a in (I, O))
+    Y = torch.empty((T, B, E), dtype=torch.float32, device=DEV)
+    Yb = torch.empty((T, B, E), dtype=torch.bfloat16, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8, device=DEV)
+    assert pk.embbag_forward_split_bf16(hi, B, Id, Od, Y, status) == 0
+    assert pk.embbag_forward_split_bf16_act(hi, B, Id, Od, Yb, status) == 0
+    assert pk.embbag_backward_prepare(cfg.rows, E, B, Id, Od, ws, status) == 0
+    if grad_bf16:
+        Gb = to_bf16_bits(G)
+        Gd = torch.from_numpy(Gb.view(np.int16)).to(DEV).view(torch.bfloat16)
+        assert pk.embbag_backward_apply_sgd_split_bf16_act(Gd, B, NS, cfg.lr, hi, lo, ws) == 0
+    else:
+        Gd = torch.from_numpy(G).to(DEV)
+        assert pk.embbag_backward_apply_sgd_split_bf16(Gd, B, NS, cfg.lr, hi, lo, ws) == 0
+    assert pk.embbag_status_read(status) == 0
+    Y = Y.cpu().numpy()
+    Yb = bf16_bits(Yb)
+    got = []
+    for t in range(T):
+        rd = torch.from_numpy(sel[t]).to(DEV)
+        got.append((hi[t][rd].cpu().numpy().view(np.uint16), lo[t][rd].cpu().numpy().view(np.uint16)))
+    del hi, lo
+    torch.cuda.empty_cache()
+
+    log(f"[full] {name}: oracle forward ({NS} look-ups)")
+    rc, Y_ref = oracle.forward_split(hi_c, B, I_c, O)
+    assert rc == 0
+    assert_close(Y, Y_ref, f"{name} pooled")
+    ndiff = assert_bf16_bracket(Yb, Y_ref, f"{name} pooled bf16")
+    log(f"[full] {name}: BF16 outputs differing from the rounded oracle value: {ndiff} of {Yb.size}")
+    if P == 1:
+        assert ndiff == 0
+    log(f"[full] {name}: oracle backward")
+    h_ref, l_ref = [h.copy() for h in hi_c], [l.copy() for l in lo_c]
+    if grad_bf16:
+        assert oracle.backward_sgd_split_bf16_act(Gb, B, I_c, O, cfg.lr, h_ref, l_ref) == 0
+    else:
+        assert oracle.backward_sgd_split(G, B, I_c, O, cfg.lr, h_ref, l_ref) == 0
+    for t in range(T):
+        is_u = np.isin(sel[t], untouched[t])
+        w_gpu = oracle.combine(*got[t])
+        w_ref = oracle.combine(h_ref[t], l_ref[t])
+        assert_close(w_gpu[~is_u], w_ref[~is_u], f"{name} table {t} touched rows")
+        assert bits_equal(got[t][0][is_u], hi_c[t][is_u]), f"{name} table {t} untouched hi changed"
+        assert bits_equal(got[t][1][is_u], lo_c[t][is_u]), f"{name} table {t} untouched lo changed"
+    log(f"[full] {name}: ok")
+
+
 def test_large_full_size():
     _run("large")
 
 
 def test_mlperf_full_size():
     _run("mlperf")
+
+
+def test_large_split_full_size():
+    _run_split("large_split", grad_bf16=False)
+
+
+def test_mlperf_split_full_size():
+    _run_split("mlperf_split", grad_bf16=True)

@@ -3,15 +3,21 @@
 Floating point: |gpu - oracle| <= 1e-6 + 1e-5 |oracle| elementwise for pooled
 outputs and updated rows; rows no look-up names must keep their bits.
 Integer work (sorted keys/bags, unique keys, segment offsets, U): bit-exact.
+BF16 pooled outputs: each value lies between the BF16 roundings of
+oracle -/+ that tolerance (rounding is monotone), and equals the rounding of
+the oracle's value wherever the sum is exact (one-term bags).
 """
+import ctypes as C
+
 import numpy as np
 import pytest
 import torch
 
 import oracle
+import paper_2005_04680_amd as pk
 from embbag_data import get_config, make_batch, make_grads, random_bags, scaled, table_values_np
-from gpu_util import (DEV, GpuTables, assert_close, bits_equal, gpu_dedup, log, require_gpu,
-                      to_dev)
+from gpu_util import (DEV, GpuTables, assert_bf16_bracket, assert_close, bf16_bits, bits_equal,
+                      gpu_dedup, log, require_gpu, to_bf16_bits, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -124,6 +130,81 @@ def test_split_full():
     I, O = make_batch(cfg, 0)
     G = make_grads(cfg, 0)
     check_step(W, cfg.batch, I, O, G, cfg.lr, split=True, what="split")
+
+
+@pytest.mark.parametrize("dim,maxp", [(16, 30), (64, 30), (128, 1), (256, 12)])
+def test_split_bf16_activations(dim, maxp):
+    """Section VII with BF16 activations: BF16 pooled outputs from the hi halves,
+    the update driven by a BF16 gradient; two-phase equals fused."""
+    rng = np.random.default_rng(900 + dim)
+    rows, batch = (3000, 1500, 700), 97 if maxp > 1 else 2000
+    W = _tables(rng, rows, dim, 0.5)
+    I, O = random_bags(rng, rows, batch, maxp, 0.1, 0.3)
+    T, NS = len(rows), I.size
+    log(f"[parity] split bf16 act E={dim} B={batch} NS={NS} P<={maxp}")
+    gt = GpuTables(W, split=True)
+    Id, Od = to_dev(I), to_dev(O)
+    Yb = torch.empty((T, batch, dim), dtype=torch.bfloat16, device=DEV)
+    assert pk.embbag_forward_split_bf16_act(gt.w, batch, Id, Od, Yb, gt.status) == 0
+    his, los = gt.host_split()
+    rc, Y32 = oracle.forward_split(his, batch, I, O)
+    assert rc == 0
+    got = bf16_bits(Yb)
+    ndiff = assert_bf16_bracket(got, Y32, f"E={dim} pooled bf16")
+    if maxp == 1:  # one-term sums are exact: every value is the rounding of the oracle's
+        rc, Yref = oracle.forward_split_bf16_act(his, batch, I, O)
+        assert rc == 0 and ndiff == 0 and np.array_equal(got, Yref)
+    Gb = to_bf16_bits(rng.standard_normal((T, batch, dim)).astype(np.float32))
+    Gd = torch.from_numpy(Gb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(T, batch, NS, dim), dtype=torch.uint8,
+                     device=DEV)
+    two = GpuTables(dev_tables=[w.clone() for w in gt.w], dev_lo=[l.clone() for l in gt.lo],
+                    split=True)
+    assert pk.embbag_backward_sgd_split_bf16_act(Gd, batch, Id, Od, 0.1, gt.w, gt.lo, ws,
+                                                 gt.status) == 0
+    assert gt.read_status() == 0
+    assert pk.embbag_backward_prepare(rows, dim, batch, Id, Od, ws, two.status) == 0
+    assert pk.embbag_backward_apply_sgd_split_bf16_act(Gd, batch, NS, 0.1, two.w, two.lo, ws) == 0
+    assert two.read_status() == 0
+    h_ref, l_ref = [h.copy() for h in his], [l.copy() for l in los]
+    assert oracle.backward_sgd_split_bf16_act(Gb, batch, I, O, 0.1, h_ref, l_ref) == 0
+    Wg, W2 = gt.host(), two.host()
+    for t in range(T):
+        Wr = oracle.combine(h_ref[t], l_ref[t])
+        touched = np.zeros(rows[t], bool)
+        touched[I[O[t * batch]:O[(t + 1) * batch]]] = True
+        assert_close(Wg[t][touched], Wr[touched], f"E={dim} table {t} touched rows")
+        assert bits_equal(Wg[t][~touched], W[t][~touched]), f"table {t} untouched rows changed"
+        assert bits_equal(W2[t], Wg[t]), f"table {t}: two-phase differs from fused"
+
+
+def test_split_bf16_activation_argument_errors():
+    rng = np.random.default_rng(950)
+    W = _tables(rng, (50,), 8, 0.5)
+    I, O = random_bags(rng, (50,), 4, 3, 0.0, 0.0)
+    gt = GpuTables(W, split=True)
+    Id, Od = to_dev(I), to_dev(O)
+    Y32 = torch.empty((1, 4, 8), dtype=torch.float32, device=DEV)
+    with pytest.raises(TypeError):  # the binding checks the dtype
+        pk.embbag_forward_split_bf16_act(gt.w, 4, Id, Od, Y32, gt.status)
+    Yb = torch.empty((1, 4, 8), dtype=torch.bfloat16, device=DEV)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(1, 4, I.size, 8), dtype=torch.uint8,
+                     device=DEV)
+    # misaligned BF16 gradient (2-byte offset) and a missing lo half are argument errors
+    Gflat = torch.zeros(1 * 4 * 8 + 1, dtype=torch.bfloat16, device=DEV)
+    lib = pk.lib()
+    s, keep = pk._tables_struct(gt.w, split_lo=gt.lo)
+    rc = lib.embbag_backward_sgd_split_bf16_act(
+        Gflat.data_ptr() + 2, 4, Id.data_ptr(), Od.data_ptr(), I.size, C.c_float(0.1), C.byref(s),
+        ws.data_ptr(), ws.numel(), None, pk._stream(None))
+    assert rc == pk.EMBBAG_ERR_INVALID_ARG
+    s2, keep2 = pk._split_struct_fwd(gt.w)  # no lo halves
+    rc = lib.embbag_backward_apply_sgd_split_bf16_act(Gflat.data_ptr(), 4, I.size, C.c_float(0.1),
+                                                      C.byref(s2), ws.data_ptr(), ws.numel(),
+                                                      pk._stream(None))
+    assert rc == pk.EMBBAG_ERR_INVALID_ARG
+    assert pk.embbag_forward_split_bf16_act(gt.w, 4, Id, Od, Yb, gt.status) == 0
+    assert gt.read_status() == 0
 
 
 # ---------------------------------------------------------------------------

@@ -406,6 +406,85 @@ def test_split_update_equals_fp32_update(oracle):
 
 
 # ----------------------------------------------------------------------------
+# BF16 activations (Section VII: forward and backward in BF16, update in FP32)
+# ----------------------------------------------------------------------------
+def _torch_bf16_bits(x):
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def _torch_bf16_widen(h):
+    return torch.from_numpy(h.view(np.int16)).view(torch.bfloat16).to(torch.float32).numpy()
+
+
+def test_bf16_round_matches_torch(oracle):
+    rng = np.random.default_rng(18)
+    ties = (rng.integers(0, 1 << 16, 50000).astype(np.uint32) << 16) | np.uint32(0x8000)
+    x = np.concatenate([
+        rng.standard_normal(200000).astype(np.float32) * np.float32(1e-3),
+        rng.integers(0, 1 << 32, 200000, dtype=np.uint64).astype(np.uint32).view(np.float32),
+        ties.view(np.float32),  # exact midpoints, odd and even last bit, both signs
+        np.float32([0.0, -0.0, np.inf, -np.inf, 3.3895314e38, 3.4028235e38, -3.4028235e38,
+                    1e-45, -1e-45, 1.1754944e-38, 1.0, -1.0]),
+    ])
+    x = x[~np.isnan(x)]
+    assert np.array_equal(oracle.bf16_round(x), _torch_bf16_bits(x))
+    # halfway between the largest finite BF16 and 2^128 rounds to infinity (ties to even)
+    assert oracle.bf16_round(np.uint32([0x7F7F8000]).view(np.float32))[0] == 0x7F80
+    assert oracle.bf16_round(np.uint32([0x7F7E8000]).view(np.float32))[0] == 0x7F7E
+    assert np.isnan(oracle.bf16_widen(oracle.bf16_round(np.float32([np.nan]))))[0]
+
+
+def test_bf16_widen_matches_torch(oracle):
+    h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    w = oracle.bf16_widen(h)
+    ref = _torch_bf16_widen(h)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(w), nan)
+    assert np.array_equal(w[~nan].view(np.uint32), ref[~nan].view(np.uint32))
+    assert np.array_equal(oracle.bf16_round(w[~nan]), h[~nan])  # BF16 values round to themselves
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_bf16_act_forward_matches_torch(oracle, case):
+    rows, dim, batch, maxp, ef, hf, seed = case
+    rng = np.random.default_rng(seed + 300)
+    W = _tables(rng, rows, dim)
+    I, O = random_bags(rng, rows, batch, maxp, ef, hf)
+    his = [oracle.split(w)[0] for w in W]
+    rc, Yb = oracle.forward_split_bf16_act(his, batch, I, O)
+    assert rc == oracle.OK and Yb.dtype == np.uint16
+    for t in range(len(rows)):
+        # sums of BF16 values (8 significant bits) over a 2^-32 range are exact in float64
+        Wt = torch.from_numpy(_torch_bf16_widen(his[t])).double()
+        lo, hi = O[t * batch], O[(t + 1) * batch]
+        idx = torch.from_numpy(I[lo:hi].astype(np.int64))
+        offs = torch.from_numpy((O[t * batch:(t + 1) * batch] - lo).astype(np.int64))
+        y = torch.nn.functional.embedding_bag(idx, Wt, offs, mode="sum").float()
+        assert np.array_equal(Yb[t], _torch_bf16_bits(y.numpy()))
+
+
+def test_bf16_act_update_uses_the_exactly_widened_gradient(oracle):
+    rng = np.random.default_rng(20)
+    rows, E, B = (60, 33), 12, 9
+    W = _tables(rng, rows, E)
+    I, O = random_bags(rng, rows, B, 8, 0.1, 0.3)
+    Gb = _torch_bf16_bits(rng.standard_normal((2, B, E)).astype(np.float32))
+    Gw = _torch_bf16_widen(Gb)
+    hi, lo = zip(*[oracle.split(w) for w in W])
+    h1, l1 = [h.copy() for h in hi], [l.copy() for l in lo]
+    assert oracle.backward_sgd_split_bf16_act(Gb, B, I, O, 0.1, h1, l1) == oracle.OK
+    # dense brute force on the widened gradient: W - lr * A^T G in float64
+    for t in range(2):
+        A = _dense_A(rows[t], B, t, I, O)
+        ref = W[t].astype(np.float64) - np.float64(np.float32(0.1)) * (A.T @ Gw[t].astype(np.float64))
+        got = oracle.combine(h1[t], l1[t])
+        touched = A.sum(axis=0) > 0
+        assert _ulp_close(got[touched], ref[touched].astype(np.float32))
+        assert np.array_equal(got[~touched].view(np.uint32), W[t][~touched].view(np.uint32))
+
+
+# ----------------------------------------------------------------------------
 # weighted and mean pooling (Section II's L = A^T W with weights a_p)
 # ----------------------------------------------------------------------------
 def _dense_A_weighted(rows_t, batch, t, indices, offsets, weights=None, mean=False):
