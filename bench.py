@@ -94,8 +94,9 @@ def unique_count(cfg, I):
     return int(sum(np.unique(I[t * n_t:(t + 1) * n_t]).size for t in range(cfg.num_tables)))
 
 
-def cpu_baseline(cfg, batch_I, G, sample_bags, act_bf16=False):
-    """The CPU oracle on the first `sample_bags` bags of every table of batch 0."""
+def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
+    """The CPU oracle on the first `sample_bags` bags of every table of each of
+    `host_batches` ((indices, grads) on the host), forward + fused backward."""
     import torch
 
     import oracle
@@ -103,41 +104,70 @@ def cpu_baseline(cfg, batch_I, G, sample_bags, act_bf16=False):
 
     P, B, T = cfg.pooling, cfg.batch, cfg.num_tables
     nb = min(sample_bags, B)
-    I_s, tabs = [], []
-    for t in range(T):
-        part = batch_I[t * B * P: t * B * P + nb * P]
-        rows, inv = np.unique(part, return_inverse=True)
-        I_s.append(inv.astype(np.int32))
-        vals = table_rows_torch(cfg.seed, t, torch.from_numpy(rows).cuda(), cfg.dim,
-                                cfg.value_scale[t])
-        tabs.append(vals.cpu().numpy())
-    I_s = np.concatenate(I_s)
-    O_s = np.arange(0, T * nb * P + 1, P, dtype=np.int32)
-    G_s = np.ascontiguousarray(G[:, :nb, :])
-    if cfg.split and act_bf16:
-        his, los = zip(*[oracle.split(w) for w in tabs])
-        his, los = list(his), list(los)
-        Gb = np.ascontiguousarray(torch.from_numpy(G_s).to(torch.bfloat16).view(torch.int16)
-                                  .numpy().view(np.uint16))
-        t0 = time.perf_counter()
-        rc1, _ = oracle.forward_split_bf16_act(his, nb, I_s, O_s)
-        rc2 = oracle.backward_sgd_split_bf16_act(Gb, nb, I_s, O_s, cfg.lr, his, los)
-    elif cfg.split:
-        his, los = zip(*[oracle.split(w) for w in tabs])
-        his, los = list(his), list(los)
-        t0 = time.perf_counter()
-        rc1, _ = oracle.forward_split(his, nb, I_s, O_s)
-        rc2 = oracle.backward_sgd_split(G_s, nb, I_s, O_s, cfg.lr, his, los)
-    else:
-        t0 = time.perf_counter()
-        rc1, _ = oracle.forward(tabs, nb, I_s, O_s)
-        rc2 = oracle.backward_sgd(G_s, nb, I_s, O_s, cfg.lr, tabs)
-    dt = time.perf_counter() - t0
-    assert rc1 == 0 and rc2 == 0
-    return {"value": I_s.size / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "sample": (f"first {nb} of {B} bags of each of the {T} tables of batch 0 "
-                       f"({I_s.size} look-ups, {sum(x.shape[0] for x in tabs)} touched rows), "
+    dt, n_look, n_rows = 0.0, 0, 0
+    for batch_I, G in host_batches:
+        I_s, tabs = [], []
+        for t in range(T):
+            part = batch_I[t * B * P: t * B * P + nb * P]
+            rows, inv = np.unique(part, return_inverse=True)
+            n_rows += rows.size
+            I_s.append(inv.astype(np.int32))
+            vals = table_rows_torch(cfg.seed, t, torch.from_numpy(rows).cuda(), cfg.dim,
+                                    cfg.value_scale[t])
+            tabs.append(vals.cpu().numpy())
+        I_s = np.concatenate(I_s)
+        O_s = np.arange(0, T * nb * P + 1, P, dtype=np.int32)
+        G_s = np.ascontiguousarray(G[:, :nb, :])
+        if cfg.split:
+            his, los = zip(*[oracle.split(w) for w in tabs])
+            his, los = list(his), list(los)
+            del tabs
+        if cfg.split and act_bf16:
+            Gb = np.ascontiguousarray(torch.from_numpy(G_s).to(torch.bfloat16).view(torch.int16)
+                                      .numpy().view(np.uint16))
+            t0 = time.perf_counter()
+            rc1, _ = oracle.forward_split_bf16_act(his, nb, I_s, O_s)
+            rc2 = oracle.backward_sgd_split_bf16_act(Gb, nb, I_s, O_s, cfg.lr, his, los)
+        elif cfg.split:
+            t0 = time.perf_counter()
+            rc1, _ = oracle.forward_split(his, nb, I_s, O_s)
+            rc2 = oracle.backward_sgd_split(G_s, nb, I_s, O_s, cfg.lr, his, los)
+        else:
+            t0 = time.perf_counter()
+            rc1, _ = oracle.forward(tabs, nb, I_s, O_s)
+            rc2 = oracle.backward_sgd(G_s, nb, I_s, O_s, cfg.lr, tabs)
+        dt += time.perf_counter() - t0
+        assert rc1 == 0 and rc2 == 0
+        n_look += I_s.size
+    return {"value": n_look / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": (f"first {nb} of {B} bags of each of the {T} tables of batches "
+                       f"0-{len(host_batches) - 1} ({n_look} look-ups, {n_rows} touched rows), "
                        f"forward + fused backward/SGD, single-threaded, {dt:.2f} s")}
+
+
+def time_graph(torch, batches, prep, fwd, apply, K, warmup):
+    """The step (prepare, forward, apply) captured once per batch as a HIP graph;
+    K replays rotating over the batches, timed with events on the replay stream."""
+    graphs = []
+    for bt in batches:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            rcs = (prep(bt), fwd(bt), apply(bt))
+        assert rcs == (0, 0, 0), rcs
+        graphs.append(g)
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        graphs[i % len(graphs)].replay()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(K):
+        graphs[i % len(graphs)].replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    del graphs
+    return {"ms_per_step": round(ms, 4), "replays": K, "graphs": len(batches)}
 
 
 def time_baselines(pk, torch, cfg, tables, batches, stream, reps=3):
@@ -185,8 +215,11 @@ def main():
     ap.add_argument("--act", default="f32", choices=["f32", "bf16"],
                     help="pooled outputs and their gradients in FP32, or in BF16 (split-storage "
                          "configurations only: Section VII's BF16 activations)")
-    ap.add_argument("--batches", type=int, default=4, help="pre-generated batches, rotated")
-    ap.add_argument("--cpu-sample-bags", type=int, default=1024)
+    ap.add_argument("--batches", type=int, default=8, help="pre-generated batches, rotated")
+    ap.add_argument("--cpu-sample-bags", type=int, default=8192,
+                    help="bags per table of each sampled batch the CPU oracle is timed on")
+    ap.add_argument("--cpu-sample-batches", type=int, default=3,
+                    help="batches the CPU oracle is timed on (about 10 s at the defaults)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--overlap-prepare", action="store_true",
                     help="run the backward's index phase on a second stream, overlapped with "
@@ -195,6 +228,9 @@ def main():
                     help="also time the paper's unfused update designs on the GPU: Algorithm 2 "
                          "(materialised dW) + Algorithm 3 (FP32 atomics), the fused atomic update, "
                          "and Algorithm 4 (row-range ownership, 256 owners)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured as one HIP graph per batch and replayed "
+                         "(for the launch-bound small workloads)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE to bytes)")
@@ -220,11 +256,19 @@ def main():
         n = 1 << 28  # 1 GiB of FP32
         src = torch.ones(n, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        dst.copy_(src)
+        e0.record()
         for _ in range(5):
             dst.copy_(src)
+        e1.record()
         torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 5
         print(json.dumps({"calibration": "copy", "bytes_read_per_copy": 4 * n,
-                          "bytes_written_per_copy": 4 * n, "copies": 5}), flush=True)
+                          "bytes_written_per_copy": 4 * n, "copies": 6,
+                          "ms_per_copy": round(ms, 4),
+                          "gbps_read_plus_write": round(8 * n / (ms * 1e-3) / 1e9, 1)}),
+              flush=True)
         return
     cfg = get_config(args.config)
     T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
@@ -261,9 +305,9 @@ def main():
         Gd = torch.from_numpy(G).to(dev)
         if act_bf16:
             Gd = Gd.to(torch.bfloat16)  # the gradient a BF16 network hands over
+        keep = b < args.cpu_sample_batches and not args.no_cpu_baseline
         batches.append(dict(I=torch.from_numpy(I).to(dev), O=torch.from_numpy(O).to(dev),
-                            G=Gd, U=U, I_host=I if b == 0 else None,
-                            G_host=G if b == 0 else None))
+                            G=Gd, U=U, I_host=I if keep else None, G_host=G if keep else None))
     log(f"[bench] {args.batches} batches generated in {time.time() - t0:.1f}s; "
         f"U = {[x['U'] for x in batches]}")
 
@@ -338,10 +382,16 @@ def main():
     prep_ms = sum(e[2].elapsed_time(e[3]) for e in ev) / K
     apply_ms = sum(e[4].elapsed_time(e[5]) for e in ev) / K
     ms_step = total_ms / K
+    # per-step times: consecutive steps partition the timed region
+    per_step = [(start if i == 0 else ev[i - 1][5]).elapsed_time(ev[i][5]) for i in range(K)]
     U_avg = sum(batches[i % len(batches)]["U"] for i in range(K)) / K
     fwd_b, bwd_b = bytes_model(cfg, U_avg, split, act_bf16)
     step_b = fwd_b + bwd_b
     gbps = step_b / (ms_step * 1e-3) / 1e9
+    # B_min: the forward counted with one read per touched row instead of one per look-up
+    sw = 2 if split else 4
+    step_min_b = step_b - (NS - U_avg) * E * sw
+    gbps_min = step_min_b / (ms_step * 1e-3) / 1e9
     # Roofline of the dominant kernel.  The forward call is one launch
     # (fwd_gather_sum); the apply call is segment_sgd plus the short
     # segment_fixup, whose events bracket both.  Algorithmic bytes per launch:
@@ -379,21 +429,26 @@ def main():
                    "pooling": cfg.pooling, "num_indices": NS, "unique_rows": round(U_avg),
                    "lr": cfg.lr, "batches_rotated": args.batches,
                    "streams": 2 if args.overlap_prepare else 1},
+        "ms_per_step_median": round(float(np.median(per_step)), 4),
+        "ms_per_step_p90": round(float(np.percentile(per_step, 90)), 4),
         "gbps_alg": round(gbps, 1),
         "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
         "bytes_alg_per_step": int(step_b),
+        "gbps_min": round(gbps_min, 1),
+        "bytes_min_per_step": int(step_min_b),
         "fwd_ms": round(fwd_ms, 4),
         "bwd_prepare_ms": round(prep_ms, 4),
         "bwd_apply_ms": round(apply_ms, 4),
         "wall_s_timed": round(wall, 3),
         "roofline": roof,
     }
+    if args.graph:
+        out["graph"] = time_graph(torch, batches, prep, fwd, apply, K, args.warmup)
     if args.baselines and not split:
         out["baselines"] = time_baselines(pk, torch, cfg, tables, batches, main)
     if not args.no_cpu_baseline:
-        b0 = batches[0]
-        out["cpu_baseline"] = cpu_baseline(cfg, b0["I_host"], b0["G_host"], args.cpu_sample_bags,
-                                           act_bf16)
+        host = [(bt["I_host"], bt["G_host"]) for bt in batches if bt["I_host"] is not None]
+        out["cpu_baseline"] = cpu_baseline(cfg, host, args.cpu_sample_bags, act_bf16)
     print(json.dumps(out), flush=True)
 
 
