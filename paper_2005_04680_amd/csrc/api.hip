@@ -147,9 +147,12 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   L.ns = NS;
   L.ntiles = (NS + kTile - 1) / kTile;
   L.nkeyblocks = L.ntiles > 0 ? L.ntiles : 1;
-  // Chunk of the segmented reduce: ~16K chunks, 64..1024 look-ups each.
-  int64_t c = 64;
-  while (c < 1024 && c * 2 * 16384 <= NS) c *= 2;
+  // Chunk of the segmented reduce: at least 128 look-ups per wavefront (a
+  // wavefront walks one chunk per row group), growing to at most 1024 while
+  // at least ~16K wavefronts remain.
+  const int64_t rgw = kWave / row_geom(E).lpr;
+  int64_t c = 128 / rgw > 8 ? 128 / rgw : 8;
+  while (c < 1024 && c * 2 * 16384 * rgw <= NS) c *= 2;
   L.chunk = c;
   L.nchunks = (NS + c - 1) / c;
   // As few passes as digits of at most 10 bits allow, the bits spread evenly
