@@ -556,6 +556,24 @@ def test_weighted_special_cases(oracle):
     assert rc == 0
     assert np.array_equal(Ym[0, 0], W[0][3]) and np.array_equal(Ym[0, 2], W[0][5])
     assert np.array_equal(Ym[0, 1].view(np.uint32), np.zeros(dim, np.uint32))
+    # a zero weight contributes nothing: same as dropping that look-up (forward and update)
+    a = rng.uniform(0.5, 2.0, I.size).astype(np.float32)
+    zero = rng.random(I.size) < 0.3
+    a[zero] = 0.0
+    keep = ~zero
+    bag = np.searchsorted(O, np.arange(I.size), side="right") - 1
+    O3 = np.zeros_like(O)
+    O3[1:] = np.cumsum(np.bincount(bag[keep], minlength=O.size - 1))
+    rc, Yz = oracle.forward_weighted(W, batch, I, O, a)
+    rc2, Yd = oracle.forward_weighted(W, batch, np.ascontiguousarray(I[keep]), O3,
+                                      np.ascontiguousarray(a[keep]))
+    assert rc == rc2 == 0 and np.array_equal(Yz.view(np.uint32), Yd.view(np.uint32))
+    Wa, Wb = [w.copy() for w in W], [w.copy() for w in W]
+    assert oracle.backward_sgd_weighted(G, batch, I, O, 0.1, Wa, a) == 0
+    assert oracle.backward_sgd_weighted(G, batch, np.ascontiguousarray(I[keep]), O3, 0.1, Wb,
+                                        np.ascontiguousarray(a[keep])) == 0
+    for a_, b_ in zip(Wa, Wb):
+        assert np.array_equal(a_.view(np.uint32), b_.view(np.uint32))
     # weights with mean pooling are rejected (torch allows weights with sum only)
     assert oracle.forward_weighted(W, batch, I, O, np.ones(I.size, np.float32),
                                    oracle.POOL_MEAN)[0] == oracle.ERR_INVALID_ARG
