@@ -94,6 +94,20 @@ def unique_count(cfg, I):
     return int(sum(np.unique(I[t * n_t:(t + 1) * n_t]).size for t in range(cfg.num_tables)))
 
 
+def host_cpu():
+    """CPU model and logical CPU count of this host (from /proc/cpuinfo)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{model}, {os.cpu_count()} logical CPUs"
+
+
 def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
     """The CPU oracle on the first `sample_bags` bags of every table of each of
     `host_batches` ((indices, grads) on the host), forward + fused backward."""
@@ -105,6 +119,10 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
     P, B, T = cfg.pooling, cfg.batch, cfg.num_tables
     nb = min(sample_bags, B)
     dt, n_look, n_rows = 0.0, 0, 0
+    # one host core for the whole timed region (the oracle is single-threaded)
+    old_aff = os.sched_getaffinity(0)
+    core = min(old_aff)
+    os.sched_setaffinity(0, {core})
     for batch_I, G in host_batches:
         I_s, tabs = [], []
         for t in range(T):
@@ -139,10 +157,12 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
         dt += time.perf_counter() - t0
         assert rc1 == 0 and rc2 == 0
         n_look += I_s.size
+    os.sched_setaffinity(0, old_aff)
     return {"value": n_look / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
             "sample": (f"first {nb} of {B} bags of each of the {T} tables of batches "
                        f"0-{len(host_batches) - 1} ({n_look} look-ups, {n_rows} touched rows), "
-                       f"forward + fused backward/SGD, single-threaded, {dt:.2f} s")}
+                       f"forward + fused backward/SGD, single-threaded, {dt:.2f} s"),
+            "host": host_cpu(), "core": core}
 
 
 def time_graph(torch, batches, prep, fwd, apply, K, warmup):
