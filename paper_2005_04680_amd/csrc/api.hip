@@ -177,6 +177,9 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   L.off_carry = take(for_dedup ? 0 : size_t(2) * size_t(L.nchunks) * size_t(E) * 8);
   L.off_uniq = take(for_dedup ? size_t(L.ntiles) * 4 : 0);
   L.off_bagof = take(for_dedup ? 0 : size_t(NS) * 4);
+  L.ngroups = (L.nchunks + kCarryGroup - 1) / kCarryGroup;
+  L.off_gsum = take(for_dedup ? 0 : size_t(L.ngroups) * size_t(E) * 8);
+  L.off_gflag = take(for_dedup ? 0 : size_t(L.ngroups) * 4);
   L.total = off;
   return L;
 }

@@ -20,6 +20,7 @@ constexpr int kMaxRadixBits = 10;
 constexpr int kMaxRadix = 1 << kMaxRadixBits;
 constexpr int kItemsPerThread = 16;
 constexpr int kTile = kBlock * kItemsPerThread;
+constexpr int kCarryGroup = 16;  // chunks per pre-summed group of carries
 
 // Sentinel for "no key": keys are < 2^31 because sum(M_t) < 2^31.
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
@@ -101,7 +102,9 @@ struct BwdLayout {
   int64_t nchunks;
   int passes;          // radix passes
   int bits;            // digit width of every pass
+  int64_t ngroups;     // groups of kCarryGroup chunks
   size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, off_bagof,
+      off_gsum, off_gflag,
       total;
 };
 

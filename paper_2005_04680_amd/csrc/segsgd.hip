@@ -279,12 +279,56 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   }
 }
 
+// Groups of kCarryGroup chunks that one segment fills entirely (the look-up
+// before the group and the one after it have the same key, so, the look-ups
+// being sorted, every look-up in between has it too): their partials (slot 2c
+// of each chunk) are summed in chunk order once, so that a long segment's
+// fixup adds one value per such group instead of one per chunk.  gflag[g]
+// says whether group g is filled (written for every group).
+template <int LPR, int CPL>
+__global__ __launch_bounds__(kBlock) void carry_group(
+    const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks, int32_t E,
+    int32_t ngroups, const double* __restrict__ carry, double* __restrict__ gsum,
+    int32_t* __restrict__ gflag, const int32_t* __restrict__ flags, uint32_t token) {
+  if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
+  constexpr int R = kWave / LPR;
+  const int E4 = E / 4;
+  const int lane = lane_id();
+  const int rg = lane / LPR, rl = lane % LPR;
+  const int g = (int(blockIdx.x) * kWavesPerBlock + wave_id()) * R + rg;
+  if (g >= ngroups) return;
+  const int64_t c0 = int64_t(g) * kCarryGroup;
+  const int64_t first = c0 * C, after = (c0 + kCarryGroup) * C;
+  const bool full = c0 > 0 && c0 + kCarryGroup <= nchunks && after < NS &&
+                    key_of(sorted[first - 1]) == key_of(sorted[after]);
+  if (rl == 0) gflag[g] = full ? 1 : 0;
+  if (!full) return;
+  d4 acc[CPL];
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) acc[j] = d4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+  for (int u = 0; u < kCarryGroup; ++u) {
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c4 = rl + j * LPR;
+      if (c4 < E4) acc[j] += *reinterpret_cast<const d4*>(carry + 2 * (c0 + u) * E + c4 * 4);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) {
+    const int c4 = rl + j * LPR;
+    if (c4 < E4) *reinterpret_cast<d4*>(gsum + int64_t(g) * E + c4 * 4) = acc[j];
+  }
+}
+
 // Segments that cross chunk boundaries: the chunk where one begins sums the
-// partials in chunk order and applies the row.
+// partials in chunk order (a filled group's pre-summed value in place of its
+// chunks) and applies the row.
 template <int LPR, int CPL, class Rows, int MODE>
 __global__ __launch_bounds__(kBlock) void segment_fixup(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     int32_t B, float inv_b, float lr, const double* __restrict__ carry,
+    const double* __restrict__ gsum, const int32_t* __restrict__ gflag,
     const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
@@ -317,16 +361,30 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
     }
   }
   // Chunks chunk+1, chunk+2, ... belong to the segment while the chunk before
-  // continues it; UF chunks (their first-segment partials and the key just
-  // past them) are loaded per step.
+  // continues it.  At a group boundary a filled group is taken whole (the
+  // segment then continues past it); otherwise up to UF chunks, not crossing
+  // the next group boundary (their first-segment partials and the key just
+  // past them), are loaded per step.
   bool inside = true;
-  for (int c2 = chunk + 1; inside; c2 += UF) {
+  int c2 = chunk + 1;
+  while (inside) {
+    const int gi = c2 / kCarryGroup, off = c2 % kCarryGroup;
+    if (off == 0 && c2 < nchunks && gflag[gi] != 0) {
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int c4 = rl + j * LPR;
+        if (c4 < E4) acc[j] += *reinterpret_cast<const d4*>(gsum + int64_t(gi) * E + c4 * 4);
+      }
+      c2 += kCarryGroup;
+      continue;
+    }
+    const int n = kCarryGroup - off < UF ? kCarryGroup - off : UF;
     d4 part[UF][CPL];
     uint32_t kn[UF];
 #pragma unroll
     for (int u = 0; u < UF; ++u) {
       const int cu = c2 + u;
-      const bool ok = cu < nchunks;
+      const bool ok = u < n && cu < nchunks;
       const int64_t nxt = int64_t(cu + 1) * C;
       kn[u] = (ok && nxt < NS) ? key_of(sorted[nxt]) : kNoKey;
 #pragma unroll
@@ -338,11 +396,12 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
     }
 #pragma unroll
     for (int u = 0; u < UF; ++u) {
-      if (!inside) break;
+      if (!inside || u >= n) break;
 #pragma unroll
       for (int j = 0; j < CPL; ++j) acc[j] += part[u][j];
       inside = kn[u] == kl;
     }
+    c2 += n;
   }
 #pragma unroll
   for (int j = 0; j < CPL; ++j) {
@@ -377,13 +436,42 @@ bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const
   return false;
 }
 
+bool launch_group(RowGeom g, hipStream_t st, const uint64_t* sorted, int32_t NS, int32_t C,
+                  int32_t nchunks, int32_t E, int32_t ngroups, const double* carry, double* gsum,
+                  int32_t* gflag, const int32_t* flags, uint32_t token) {
+  const int per_block = kWavesPerBlock * (kWave / g.lpr);
+  const int blocks = (ngroups + per_block - 1) / per_block;
+  if (blocks == 0) return true;
+#define EMB_GRP(L, CC)                                                                        \
+  hipLaunchKernelGGL((carry_group<L, CC>), dim3(blocks), dim3(kBlock), 0, st, sorted, NS, C, \
+                     nchunks, E, ngroups, carry, gsum, gflag, flags, token)
+  switch (g.lpr) {
+    case 1: EMB_GRP(1, 1); return true;
+    case 2: EMB_GRP(2, 1); return true;
+    case 4: EMB_GRP(4, 1); return true;
+    case 8: EMB_GRP(8, 1); return true;
+    case 16: EMB_GRP(16, 1); return true;
+    case 32: EMB_GRP(32, 1); return true;
+    case 64:
+      switch (g.cpl) {
+        case 1: EMB_GRP(64, 1); return true;
+        case 2: EMB_GRP(64, 2); return true;
+        case 3: EMB_GRP(64, 3); return true;
+        case 4: EMB_GRP(64, 4); return true;
+      }
+  }
+#undef EMB_GRP
+  return false;
+}
+
 template <class Rows, int MODE>
 bool launch_fix(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
                 int32_t NS, int32_t C, int32_t nchunks, int32_t B, float inv_b, float lr,
-                const double* carry, const int32_t* flags, uint32_t token, PoolDev pd) {
+                const double* carry, const double* gsum, const int32_t* gflag,
+                const int32_t* flags, uint32_t token, PoolDev pd) {
 #define EMB_FIX(L, CC)                                                                       \
   hipLaunchKernelGGL((segment_fixup<L, CC, Rows, MODE>), dim3(blocks), dim3(kBlock), 0, st, d, \
-                     sorted, NS, C, nchunks, B, inv_b, lr, carry, flags, token, pd)
+                     sorted, NS, C, nchunks, B, inv_b, lr, carry, gsum, gflag, flags, token, pd)
   switch (g.lpr) {
     case 1: EMB_FIX(1, 1); return true;
     case 2: EMB_FIX(2, 1); return true;
@@ -408,6 +496,8 @@ bool launch_apply(const TableDesc& d, int32_t B, const void* dY, float lr, const
                   char* ws, uint32_t token, PoolDev pd, hipStream_t st) {
   const uint64_t* sorted = sorted_buffer(L, ws);
   double* carry = reinterpret_cast<double*>(ws + L.off_carry);
+  double* gsum = reinterpret_cast<double*>(ws + L.off_gsum);
+  int32_t* gflag = reinterpret_cast<int32_t*>(ws + L.off_gflag);
   const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
   const float inv_b = 1.0f / float(B);
   const RowGeom g = row_geom(d.dim);
@@ -416,8 +506,10 @@ bool launch_apply(const TableDesc& d, int32_t B, const void* dY, float lr, const
   const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
   return launch_seg<Rows, MODE, GBF16>(g, blocks, st, d, sorted, NS, C, nch, dY, B, inv_b, lr,
                                        carry, flags, token, pd) &&
-         launch_fix<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry, flags,
-                                token, pd);
+         launch_group(g, st, sorted, NS, C, nch, d.dim, int32_t(L.ngroups), carry, gsum, gflag,
+                      flags, token) &&
+         launch_fix<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry, gsum,
+                                gflag, flags, token, pd);
 }
 
 }  // namespace

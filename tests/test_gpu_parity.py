@@ -112,6 +112,27 @@ def test_many_tiles_and_long_segments(pool, batch, hot):
     check_step(W, batch, I, O, G, 0.1, what=f"tiles P<={pool}")
 
 
+@pytest.mark.parametrize("dim,seed", [(16, 1), (64, 2), (64, 3), (256, 4)])
+def test_segments_of_many_lengths(dim, seed):
+    """Segments of every length from 1 to tens of thousands of look-ups, in random
+    bags: they start and end at every offset within chunks and within the groups
+    of chunks whose partials are pre-summed, and some fill several whole groups."""
+    rng = np.random.default_rng(1000 + seed)
+    M = 400
+    mult = np.concatenate([rng.integers(1, 40, 200), rng.integers(40, 3000, 40),
+                           rng.integers(3000, 40000, 6)])
+    rows_used = rng.permutation(M)[:mult.size]
+    look = np.repeat(rows_used, mult).astype(np.int32)
+    rng.shuffle(look)
+    NS = look.size
+    batch = NS // 37 + 1
+    cuts = np.sort(rng.integers(0, NS + 1, batch - 1))
+    O = np.concatenate([[0], cuts, [NS]]).astype(np.int32)
+    W = _tables(rng, (M,), dim, 0.01)
+    G = rng.standard_normal((1, batch, dim)).astype(np.float32)
+    check_step(W, batch, look, O, G, 0.1, what=f"segment lengths E={dim}")
+
+
 def test_small_full():
     """Small-shaped workload at full size: 8 x 1e6 x 64, B=2048, P=32, Zipf(1.05)."""
     cfg = get_config("small")
