@@ -145,7 +145,24 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   (void)B;
   BwdLayout L{};
   L.ns = NS;
-  L.ntiles = (NS + kTile - 1) / kTile;
+  // As few passes as digits of at most 10 bits allow, the bits spread evenly
+  // over them (27-bit keys: 3 passes of 9 bits).
+  int nbits = 0;
+  if (total_rows > 1) nbits = 32 - __builtin_clz(total_rows - 1u);
+  L.passes = (nbits + kMaxRadixBits - 1) / kMaxRadixBits;
+  L.bits = L.passes > 0 ? (nbits + L.passes - 1) / L.passes : 6;
+  if (L.bits < 6) L.bits = 6;
+  // Radix tiles: the largest of 4096, 2048 or 1024 keys that still gives at
+  // least 512 tiles (two per compute unit), but at least 4 keys per digit
+  // value (a tile's scatter then writes runs, not single words).  Sizes only
+  // shrink as the key width grows, so the workspace computed without the
+  // table sizes (6-bit digits) covers every call.
+  const int ipt_min = (1 << L.bits) / 64 > 4 ? (1 << L.bits) / 64 : 4;
+  L.ipt = kMaxItemsPerThread;
+  while (L.ipt > ipt_min &&
+         (NS + int64_t(kBlock) * L.ipt - 1) / (int64_t(kBlock) * L.ipt) < 512)
+    L.ipt /= 2;
+  L.ntiles = (NS + int64_t(kBlock) * L.ipt - 1) / (int64_t(kBlock) * L.ipt);
   L.nkeyblocks = L.ntiles > 0 ? L.ntiles : 1;
   // Chunk of the segmented reduce: at least 128 look-ups per wavefront (a
   // wavefront walks one chunk per row group), growing to at most 1024 while
@@ -155,13 +172,6 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   while (c < 1024 && c * 2 * 16384 * rgw <= NS) c *= 2;
   L.chunk = c;
   L.nchunks = (NS + c - 1) / c;
-  // As few passes as digits of at most 10 bits allow, the bits spread evenly
-  // over them (27-bit keys: 3 passes of 9 bits).
-  int nbits = 0;
-  if (total_rows > 1) nbits = 32 - __builtin_clz(total_rows - 1u);
-  L.passes = (nbits + kMaxRadixBits - 1) / kMaxRadixBits;
-  L.bits = L.passes > 0 ? (nbits + L.passes - 1) / L.passes : 6;
-  if (L.bits < 6) L.bits = 6;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;

@@ -14,12 +14,11 @@ constexpr int kBlock = 256;        // threads per workgroup (4 waves)
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kNumXcd = 8;         // MI355X: 8 XCDs, each with its own L2
 
-// Radix sort geometry: digits of 6..10 bits, 4096-key tiles (256 threads x
-// 16 keys).
+// Radix sort geometry: digits of 6..10 bits, tiles of 256 threads x 4, 8 or
+// 16 keys.
 constexpr int kMaxRadixBits = 10;
 constexpr int kMaxRadix = 1 << kMaxRadixBits;
-constexpr int kItemsPerThread = 16;
-constexpr int kTile = kBlock * kItemsPerThread;
+constexpr int kMaxItemsPerThread = 16;  // radix tile: kBlock * (4, 8 or 16) keys
 constexpr int kCarryGroup = 16;  // chunks per pre-summed group of carries
 
 // Sentinel for "no key": keys are < 2^31 because sum(M_t) < 2^31.
@@ -96,7 +95,8 @@ struct PoolArgs {
 // ---- launchers (host) ------------------------------------------------------
 struct BwdLayout {
   int64_t ns;
-  int64_t ntiles;      // radix tiles of kTile keys
+  int ipt;             // keys per thread of a radix tile (4, 8 or 16)
+  int64_t ntiles;      // radix tiles of kBlock * ipt keys
   int64_t nkeyblocks;  // blocks of the key-build kernel
   int64_t chunk;       // sorted look-ups per segment-reduce chunk
   int64_t nchunks;

@@ -8,7 +8,8 @@
 // reduce-then-scan, one pass per digit of BITS = 6..10 bits (as few passes as
 // the key width allows: 3 for 27- or 28-bit keys): a per-tile digit
 // histogram, a scan per digit over the tiles, and a scatter in which every
-// 4096-key tile is ranked in LDS (wavefront ballots give each lane its rank
+// tile (1024, 2048 or 4096 keys: the largest that still gives two tiles per
+// compute unit) is ranked in LDS (wavefront ballots give each lane its rank
 // among equal digits) and written out in digit order, so that the global
 // stores form runs of consecutive addresses.  No kernel waits on another
 // workgroup.
@@ -59,13 +60,14 @@ struct Radix {
 
 // Bags, keys and the first digit's histogram for one tile; offsets checks for
 // a slice of the bags; one status word per block.
-template <int BITS>
+template <int BITS, int IPT>
 __global__ __launch_bounds__(kBlock) void build_keys(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, float inv_b, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
     uint32_t* __restrict__ hist, int32_t* __restrict__ parts, uint32_t* __restrict__ bagof) {
   constexpr int R = Radix<BITS>::R;
-  __shared__ uint32_t lbag[kTile];
+  constexpr int TILE = kBlock * IPT;
+  __shared__ uint32_t lbag[TILE];
   __shared__ uint32_t lhist[R];
   __shared__ int32_t lerr;
   __shared__ int32_t krange[2];
@@ -84,10 +86,10 @@ __global__ __launch_bounds__(kBlock) void build_keys(
     if (k < TB && O[k + 1] < o) err = EMBBAG_ERR_OFFSETS;
   }
 
-  const int s_lo = blk * kTile;
-  const int s_hi = min(s_lo + kTile, NS);
+  const int s_lo = blk * TILE;
+  const int s_hi = min(s_lo + TILE, NS);
   if (s_lo < s_hi) {  // uniform over the block
-    for (int i = tid; i < kTile; i += kBlock) lbag[i] = 0;
+    for (int i = tid; i < TILE; i += kBlock) lbag[i] = 0;
     if (tid < 2) {
       // last bag k in [0, TB - 1] with O[k] <= x (binary search; O monotone
       // when valid, and clamped so a bad O still stays in bounds)
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(kBlock) void build_keys(
     }
     __syncthreads();
 #pragma unroll 4
-    for (int i = 0; i < kItemsPerThread; ++i) {
+    for (int i = 0; i < IPT; ++i) {
       const int s = s_lo + i * kBlock + tid;
       uint32_t key = 0;
       if (s < s_hi) {
@@ -137,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void build_keys(
 }
 
 // Digit histogram of one tile of the current arrangement.
-template <int BITS>
+template <int BITS, int IPT>
 __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restrict__ src,
                                                         int32_t NS, int shift, int32_t ntiles,
                                                         uint32_t* __restrict__ hist) {
@@ -146,9 +148,9 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restri
   const int tid = threadIdx.x, blk = blockIdx.x;
   for (int i = tid; i < R; i += kBlock) lhist[i] = 0;
   __syncthreads();
-  const int base = blk * kTile;
+  const int base = blk * (kBlock * IPT);
 #pragma unroll 4
-  for (int i = 0; i < kItemsPerThread; ++i) {
+  for (int i = 0; i < IPT; ++i) {
     const int s = base + i * kBlock + tid;
     if (s < NS) atomicAdd(&lhist[(key_of(src[s]) >> shift) & (R - 1)], 1u);
   }
@@ -197,13 +199,14 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
 }
 
 // Stable scatter of one tile by the digit at `shift`.
-template <int BITS>
+template <int BITS, int IPT>
 __global__ __launch_bounds__(kBlock) void radix_downsweep(
     const uint64_t* __restrict__ src, uint64_t* __restrict__ dst, int32_t NS, int shift,
     int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals) {
   constexpr int R = Radix<BITS>::R;
   constexpr int DPT = Radix<BITS>::DPT;
-  __shared__ uint64_t buf[kTile];
+  constexpr int TILE = kBlock * IPT;
+  __shared__ uint64_t buf[TILE];
   __shared__ uint32_t whist[kWavesPerBlock][R];
   __shared__ uint32_t lstart[R];
   __shared__ uint32_t gbase[R];
@@ -234,20 +237,20 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   for (int i = tid; i < kWavesPerBlock * R; i += kBlock) (&whist[0][0])[i] = 0;
   __syncthreads();
 
-  // Wave w owns keys [w*1024, (w+1)*1024) of the tile, item i of lane l being
-  // key w*1024 + i*64 + l: ranking item by item keeps the original order.
-  const int wbase = blk * kTile + w * (kWave * kItemsPerThread);
-  uint64_t item[kItemsPerThread];
-  uint32_t dig[kItemsPerThread];
-  uint32_t rank[kItemsPerThread];
+  // Wave w owns keys [w*64*IPT, (w+1)*64*IPT) of the tile, item i of lane l
+  // being key w*64*IPT + i*64 + l: ranking item by item keeps the original order.
+  const int wbase = blk * TILE + w * (kWave * IPT);
+  uint64_t item[IPT];
+  uint32_t dig[IPT];
+  uint32_t rank[IPT];
 #pragma unroll
-  for (int i = 0; i < kItemsPerThread; ++i) {
+  for (int i = 0; i < IPT; ++i) {
     const int pos = wbase + i * kWave + lane;
     item[i] = pos < NS ? src[pos] : ~0ull;
   }
   const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
-  for (int i = 0; i < kItemsPerThread; ++i) {
+  for (int i = 0; i < IPT; ++i) {
     const bool valid = wbase + i * kWave + lane < NS;
     const uint32_t dg = (key_of(item[i]) >> shift) & (R - 1);
     dig[i] = dg;
@@ -295,11 +298,11 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kItemsPerThread; ++i) {
+  for (int i = 0; i < IPT; ++i) {
     if (wbase + i * kWave + lane < NS) buf[lstart[dig[i]] + whist[w][dig[i]] + rank[i]] = item[i];
   }
   __syncthreads();
-  const int nvalid = min(kTile, NS - blk * kTile);
+  const int nvalid = min(TILE, NS - blk * TILE);
   for (int j = tid; j < nvalid; j += kBlock) {
     const uint64_t it = buf[j];
     const uint32_t dg = (key_of(it) >> shift) & (R - 1);
@@ -310,6 +313,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
 // ---- unique keys and segment offsets (checking entry point only) ----------
 
 // Unpacks one tile and counts its segment heads.
+template <int IPT>
 __global__ __launch_bounds__(kBlock) void unique_count(const uint64_t* __restrict__ sorted,
                                                        int32_t NS, uint32_t* __restrict__ skeys,
                                                        uint32_t* __restrict__ sbags,
@@ -317,8 +321,8 @@ __global__ __launch_bounds__(kBlock) void unique_count(const uint64_t* __restric
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   const int tid = threadIdx.x, blk = blockIdx.x;
   uint32_t c = 0;
-  for (int i = 0; i < kItemsPerThread; ++i) {
-    const int s = blk * kTile + i * kBlock + tid;
+  for (int i = 0; i < IPT; ++i) {
+    const int s = blk * (kBlock * IPT) + i * kBlock + tid;
     if (s < NS) {
       const uint64_t p = sorted[s];
       skeys[s] = key_of(p);
@@ -354,6 +358,7 @@ __global__ __launch_bounds__(kBlock) void unique_scan(uint32_t* __restrict__ cou
 }
 
 // Writes unique_keys[u] and seg_off[u] for the heads of one tile, in order.
+template <int IPT>
 __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restrict__ sorted,
                                                        int32_t NS,
                                                        const uint32_t* __restrict__ tile_off,
@@ -362,8 +367,8 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   const int tid = threadIdx.x, blk = blockIdx.x;
   uint32_t running = tile_off[blk];
-  for (int i = 0; i < kItemsPerThread; ++i) {
-    const int s = blk * kTile + i * kBlock + tid;
+  for (int i = 0; i < IPT; ++i) {
+    const int s = blk * (kBlock * IPT) + i * kBlock + tid;
     bool head = false;
     uint32_t key = 0;
     if (s < NS) {
@@ -380,7 +385,7 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
   }
 }
 
-template <int BITS>
+template <int BITS, int IPT>
 hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
                        uint32_t token, bool by_lookup, hipStream_t st) {
@@ -397,7 +402,7 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   const int ntiles = int(L.ntiles);
   const float inv_b = B > 0 ? 1.0f / float(B) : 0.0f;
   uint32_t* bagof = by_lookup ? reinterpret_cast<uint32_t*>(ws + L.off_bagof) : nullptr;
-  hipLaunchKernelGGL(build_keys<BITS>, dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B,
+  hipLaunchKernelGGL((build_keys<BITS, IPT>), dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B,
                      inv_b, TB, ntiles, vb, a, hist, parts, bagof);
   // Status verdict (block R of the first scan, or alone when nothing is sorted).
   const int passes = NS > 0 ? L.passes : 0;
@@ -411,11 +416,11 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   for (int p = 0; p < passes; ++p) {
     const int shift = p * BITS;
     if (p > 0)
-      hipLaunchKernelGGL(radix_upsweep<BITS>, dim3(ntiles), dim3(kBlock), 0, st, src,
+      hipLaunchKernelGGL((radix_upsweep<BITS, IPT>), dim3(ntiles), dim3(kBlock), 0, st, src,
                          int32_t(NS), shift, ntiles, hist);
     hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? R + 1 : R), dim3(kBlock), 0, st, hist, ntiles, R,
                        totals, parts, nkb, flags, d_status, token);
-    hipLaunchKernelGGL(radix_downsweep<BITS>, dim3(ntiles), dim3(kBlock), 0, st, src, dst,
+    hipLaunchKernelGGL((radix_downsweep<BITS, IPT>), dim3(ntiles), dim3(kBlock), 0, st, src, dst,
                        int32_t(NS), shift, ntiles, hist, totals);
     uint64_t* tmp = src;
     src = dst;
@@ -424,17 +429,42 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   return hipGetLastError();
 }
 
+template <int BITS>
+hipError_t sort_ipt(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O, int64_t NS,
+                    const BwdLayout& L, char* ws, int32_t* d_status, uint32_t token,
+                    bool by_lookup, hipStream_t st) {
+  switch (L.ipt) {
+    case 4: return sort_passes<BITS, 4>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 8: return sort_passes<BITS, 8>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 16: return sort_passes<BITS, 16>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int IPT>
+void unique_launch(const uint64_t* sorted, const BwdLayout& L, uint32_t* counts,
+                   uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,
+                   int32_t* seg_off, int32_t* d_num_unique, hipStream_t st) {
+  const int ntiles = int(L.ntiles);
+  hipLaunchKernelGGL(unique_count<IPT>, dim3(ntiles), dim3(kBlock), 0, st, sorted, int32_t(L.ns),
+                     sorted_keys, sorted_bags, counts);
+  hipLaunchKernelGGL(unique_scan, dim3(1), dim3(kBlock), 0, st, counts, ntiles, int32_t(L.ns),
+                     seg_off, d_num_unique);
+  hipLaunchKernelGGL(unique_write<IPT>, dim3(ntiles), dim3(kBlock), 0, st, sorted, int32_t(L.ns),
+                     counts, unique_keys, seg_off);
+}
+
 }  // namespace
 
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
                        uint32_t token, bool by_lookup, hipStream_t st) {
   switch (L.bits) {
-    case 6: return sort_passes<6>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 7: return sort_passes<7>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 8: return sort_passes<8>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 9: return sort_passes<9>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 10: return sort_passes<10>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 6: return sort_ipt<6>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 7: return sort_ipt<7>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 8: return sort_ipt<8>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 9: return sort_ipt<9>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 10: return sort_ipt<10>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
   }
   return hipErrorInvalidValue;
 }
@@ -443,18 +473,20 @@ hipError_t launch_unique(const uint64_t* sorted, const BwdLayout& L, char* ws,
                          uint32_t* sorted_keys, uint32_t* sorted_bags, uint32_t* unique_keys,
                          int32_t* seg_off, int32_t* d_num_unique, hipStream_t st) {
   uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.off_uniq);
-  const int ntiles = int(L.ntiles);
   if (L.ns == 0) {
     hipLaunchKernelGGL(unique_scan, dim3(1), dim3(kBlock), 0, st, counts, 0, 0, seg_off,
                        d_num_unique);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(unique_count, dim3(ntiles), dim3(kBlock), 0, st, sorted, int32_t(L.ns),
-                     sorted_keys, sorted_bags, counts);
-  hipLaunchKernelGGL(unique_scan, dim3(1), dim3(kBlock), 0, st, counts, ntiles, int32_t(L.ns),
-                     seg_off, d_num_unique);
-  hipLaunchKernelGGL(unique_write, dim3(ntiles), dim3(kBlock), 0, st, sorted, int32_t(L.ns),
-                     counts, unique_keys, seg_off);
+  switch (L.ipt) {
+    case 4: unique_launch<4>(sorted, L, counts, sorted_keys, sorted_bags, unique_keys, seg_off,
+                             d_num_unique, st); break;
+    case 8: unique_launch<8>(sorted, L, counts, sorted_keys, sorted_bags, unique_keys, seg_off,
+                             d_num_unique, st); break;
+    case 16: unique_launch<16>(sorted, L, counts, sorted_keys, sorted_bags, unique_keys, seg_off,
+                               d_num_unique, st); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -231,7 +231,8 @@ def test_split_bf16_activation_argument_errors():
 # ---------------------------------------------------------------------------
 # Integer work: bit-exact
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("case", ["tiny", "random", "p1_hot", "small", "mlperf_scaled"])
+@pytest.mark.parametrize("case", ["tiny", "random", "p1_hot", "small", "mlperf_scaled",
+                                  "tile1024", "tile2048", "tile4096"])
 def test_dedup_bit_exact(case):
     rng = np.random.default_rng(5)
     if case == "tiny":
@@ -248,10 +249,17 @@ def test_dedup_bit_exact(case):
         cfg = get_config("small")
         rows, batch = cfg.rows, cfg.batch
         I, O = make_batch(cfg, 1)
-    else:
+    elif case == "mlperf_scaled":
         cfg = scaled(get_config("mlperf"), batch=8192)
         rows, batch = cfg.rows, cfg.batch
         I, O = make_batch(cfg, 0)
+    else:
+        # radix tiles of 1024, 2048 and 4096 keys: 12-bit keys (6-bit digits)
+        # over 300K look-ups; 17-bit keys (9-bit digits) over 400K and 3M
+        rows, batch, pool = {"tile1024": ((3000, 1000), 10000, 60),
+                             "tile2048": ((100000, 31072), 8000, 100),
+                             "tile4096": ((100000, 31072), 30000, 200)}[case]
+        I, O = random_bags(rng, rows, batch, pool, 0.05, 0.3)
     log(f"[dedup] {case} NS={I.size}")
     rc, d_ref = oracle.dedup(rows, batch, I, O)
     assert rc == 0
