@@ -414,7 +414,7 @@ def main():
     gbps_min = step_min_b / (ms_step * 1e-3) / 1e9
     # Roofline of the dominant kernel.  The forward call is one launch
     # (fwd_gather_sum); the apply call is segment_sgd plus the short
-    # segment_fixup, whose events bracket both.  Algorithmic bytes per launch:
+    # carry_group and segment_fixup, whose events bracket all three.  Algorithmic bytes per launch:
     # forward = NS*E*s_w + 4*NS + 4*(TB+1) + s_y*TB*E (every look-up reads its
     # row); apply = dY once (s_y*TB*E) + the sorted look-ups (8*NS) + one read
     # and one write of every touched row (2*U*E*4).
@@ -422,7 +422,8 @@ def main():
     sy = 2 if act_bf16 else 4
     apply_b = sy * TB * E + 8 * NS + 2 * U_avg * E * 4
     if apply_ms >= fwd_ms:
-        roof_call, roof_k, roof_b, roof_ms = "apply", "segment_sgd+segment_fixup", apply_b, apply_ms
+        roof_call, roof_k, roof_b, roof_ms = ("apply", "segment_sgd+carry_group+segment_fixup",
+                                              apply_b, apply_ms)
     else:
         roof_call, roof_k, roof_b, roof_ms = "forward", "fwd_gather_sum", fwd_b, fwd_ms
     achieved = roof_b / (roof_ms * 1e-3) / 1e9
