@@ -153,7 +153,7 @@ def test_split_full():
     check_step(W, cfg.batch, I, O, G, cfg.lr, split=True, what="split")
 
 
-@pytest.mark.parametrize("dim,maxp", [(16, 30), (64, 30), (128, 1), (256, 12)])
+@pytest.mark.parametrize("dim,maxp", [(16, 30), (64, 30), (128, 1), (256, 12), (1024, 5)])
 def test_split_bf16_activations(dim, maxp):
     """Section VII with BF16 activations: BF16 pooled outputs from the hi halves,
     the update driven by a BF16 gradient; two-phase equals fused."""
@@ -342,6 +342,59 @@ def test_index_out_of_range_is_reported_and_writes_nothing():
     gt.reset_status()
     assert gt.backward(G, 50, I, O, 0.1) == 0
     assert gt.read_status() == oracle.ERR_INDEX_RANGE
+
+
+@pytest.mark.parametrize("kind", ["index", "offsets"])
+def test_data_errors_on_the_split_and_bf16_paths_write_nothing(kind):
+    rng = np.random.default_rng(13)
+    rows, E, B = (100, 20), 64, 50
+    W = _tables(rng, rows, E, 0.1)
+    I, O = random_bags(rng, rows, B, 10, 0.0, 0.0)
+    if kind == "index":
+        I[O[60] + 1] = 20       # row 20 of a 20-row table
+        expect = oracle.ERR_INDEX_RANGE
+    else:
+        O[30] = O[31] + 1       # decreasing offsets
+        expect = oracle.ERR_OFFSETS
+    assert oracle.validate(rows, E, B, I, O) == expect
+    gt = GpuTables(W, split=True)
+    his0, los0 = gt.host_split()
+    Id, Od = to_dev(I), to_dev(O)
+    Gb = to_bf16_bits(rng.standard_normal((2, B, E)).astype(np.float32))
+    Gd = torch.from_numpy(Gb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(2, B, I.size, E), dtype=torch.uint8,
+                     device=DEV)
+    Yb = torch.empty((2, B, E), dtype=torch.bfloat16, device=DEV)
+    assert pk.embbag_forward_split_bf16_act(gt.w, B, Id, Od, Yb, gt.status) == 0
+    assert gt.read_status() == expect
+    gt.reset_status()
+    assert pk.embbag_backward_sgd_split_bf16_act(Gd, B, Id, Od, 0.1, gt.w, gt.lo, ws,
+                                                 gt.status) == 0
+    assert gt.read_status() == expect
+    gt.reset_status()
+    assert gt.backward(make_grads_like(rng, 2, B, E), B, I, O, 0.1) == 0
+    assert gt.read_status() == expect
+    his, los = gt.host_split()
+    for a, b, c, d in zip(his, his0, los, los0):
+        assert bits_equal(a, b) and bits_equal(c, d)
+
+
+def make_grads_like(rng, T, B, E):
+    return rng.standard_normal((T, B, E)).astype(np.float32)
+
+
+@pytest.mark.parametrize("dim", [8, 1024])
+def test_sixty_four_tables(dim):
+    """The largest table count the boundary accepts, tables of 1 to 5000 rows."""
+    rng = np.random.default_rng(64 + dim)
+    rows = tuple(int(m) for m in rng.integers(1, 5000, 64))
+    rows = (1,) + rows[1:]
+    batch = 40
+    W = _tables(rng, rows, dim, 0.05)
+    I, O = random_bags(rng, rows, batch, 12, 0.1, 0.2)
+    G = rng.standard_normal((64, batch, dim)).astype(np.float32)
+    check_step(W, batch, I, O, G, 0.1, what=f"64 tables E={dim}")
+    check_step(W, batch, I, O, G, 0.1, split=True, what=f"64 split tables E={dim}")
 
 
 @pytest.mark.parametrize("kind", ["first", "decreasing", "last", "both"])
