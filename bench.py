@@ -34,9 +34,11 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def describe(cfg, act_bf16=False):
+def describe(cfg, act_bf16=False, pooling="sum"):
     kind = "split-BF16 hi/lo" if cfg.split else "FP32"
     act = ", BF16 pooled outputs and gradients" if act_bf16 else ""
+    act += {"sum": "", "weighted": ", weighted sum (per-look-up weights U(0.5, 1.5))",
+            "mean": ", mean pooling"}[pooling]
     if cfg.name.startswith("mlperf"):
         return (f"{cfg.name}: 26 tables, log-uniform rows in [10, 4e7], {kind} "
                 f"({cfg.table_bytes / 1e9:.1f} GB), E=128, batch 65536, 1 look-up/bag, "
@@ -47,7 +49,7 @@ def describe(cfg, act_bf16=False):
             f"{dist}{act}")
 
 
-def bytes_model(cfg, U, split, act_bf16=False):
+def bytes_model(cfg, U, split, act_bf16=False, weighted=False):
     """Algorithmic HBM bytes of one step (forward, backward+update).  Row reads of
     the forward are s_w = 4 B (FP32) or 2 B (BF16 hi halves) per element; pooled
     outputs and their gradients s_y = 4 B or 2 B (BF16 activations); the update
@@ -58,6 +60,9 @@ def bytes_model(cfg, U, split, act_bf16=False):
     sy = 2 if act_bf16 else 4
     fwd = NS * E * sw + 4 * NS + 4 * (TB + 1) + sy * TB * E
     bwd = sy * TB * E + 4 * NS + 4 * (TB + 1) + 2 * U * E * 4
+    if weighted:  # one weight per look-up, read by the forward and by the update
+        fwd += 4 * NS
+        bwd += 4 * NS
     return fwd, bwd
 
 
@@ -84,8 +89,8 @@ def profiled_traffic(workload, call):
     return r["fetch_bytes"] + r["write_bytes"]
 
 
-def workload_tag(cfg, act_bf16):
-    return cfg.name + ("+bf16act" if act_bf16 else "")
+def workload_tag(cfg, act_bf16, pooling="sum"):
+    return cfg.name + ("+bf16act" if act_bf16 else "") + ("" if pooling == "sum" else "+" + pooling)
 
 
 def unique_count(cfg, I):
@@ -108,9 +113,10 @@ def host_cpu():
     return f"{model}, {os.cpu_count()} logical CPUs"
 
 
-def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
+def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
     """The CPU oracle on the first `sample_bags` bags of every table of each of
-    `host_batches` ((indices, grads) on the host), forward + fused backward."""
+    `host_batches` ((indices, grads, weights or None) on the host), forward +
+    fused backward."""
     import torch
 
     import oracle
@@ -123,13 +129,15 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
     old_aff = os.sched_getaffinity(0)
     core = min(old_aff)
     os.sched_setaffinity(0, {core})
-    for batch_I, G in host_batches:
-        I_s, tabs = [], []
+    for batch_I, G, A in host_batches:
+        I_s, tabs, A_s = [], [], []
         for t in range(T):
             part = batch_I[t * B * P: t * B * P + nb * P]
             rows, inv = np.unique(part, return_inverse=True)
             n_rows += rows.size
             I_s.append(inv.astype(np.int32))
+            if A is not None:
+                A_s.append(A[t * B * P: t * B * P + nb * P])
             vals = table_rows_torch(cfg.seed, t, torch.from_numpy(rows).cuda(), cfg.dim,
                                     cfg.value_scale[t])
             tabs.append(vals.cpu().numpy())
@@ -150,6 +158,12 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False):
             t0 = time.perf_counter()
             rc1, _ = oracle.forward_split(his, nb, I_s, O_s)
             rc2 = oracle.backward_sgd_split(G_s, nb, I_s, O_s, cfg.lr, his, los)
+        elif pooling != "sum":
+            mode = oracle.POOL_MEAN if pooling == "mean" else oracle.POOL_SUM
+            a = np.ascontiguousarray(np.concatenate(A_s)) if A_s else None
+            t0 = time.perf_counter()
+            rc1, _ = oracle.forward_weighted(tabs, nb, I_s, O_s, a, mode)
+            rc2 = oracle.backward_sgd_weighted(G_s, nb, I_s, O_s, cfg.lr, tabs, a, mode)
         else:
             t0 = time.perf_counter()
             rc1, _ = oracle.forward(tabs, nb, I_s, O_s)
@@ -232,6 +246,9 @@ def main():
     ap.add_argument("--config", default="large",
                     choices=["tiny", "small", "large", "mlperf", "split", "large_split",
                              "mlperf_split", "small_p50_uniform", "large_uniform"])
+    ap.add_argument("--pooling", default="sum", choices=["sum", "weighted", "mean"],
+                    help="sum (the paper's default), weighted sum with per-look-up weights "
+                         "U(0.5, 1.5), or mean (FP32 tables only)")
     ap.add_argument("--act", default="f32", choices=["f32", "bf16"],
                     help="pooled outputs and their gradients in FP32, or in BF16 (split-storage "
                          "configurations only: Section VII's BF16 activations)")
@@ -266,7 +283,8 @@ def main():
     import torch
 
     import paper_2005_04680_amd as pk
-    from embbag_data import fill_table_torch, fill_tables_torch, get_config, make_batch, make_grads
+    from embbag_data import (fill_table_torch, fill_tables_torch, get_config, make_batch,
+                             make_grads, make_weights)
 
     pk.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -297,6 +315,11 @@ def main():
     if act_bf16 and not split:
         print(json.dumps({"error": "--act bf16 needs a split-storage configuration"}))
         sys.exit(2)
+    pooled = args.pooling != "sum"
+    if pooled and split:
+        print(json.dumps({"error": "--pooling weighted/mean runs on FP32 tables"}))
+        sys.exit(2)
+    pool_code = pk.EMBBAG_POOL_MEAN if args.pooling == "mean" else pk.EMBBAG_POOL_SUM
 
     # ---- tables in HBM ----------------------------------------------------
     t0 = time.time()
@@ -326,8 +349,11 @@ def main():
         if act_bf16:
             Gd = Gd.to(torch.bfloat16)  # the gradient a BF16 network hands over
         keep = b < args.cpu_sample_batches and not args.no_cpu_baseline
+        A = make_weights(cfg, b) if args.pooling == "weighted" else None
         batches.append(dict(I=torch.from_numpy(I).to(dev), O=torch.from_numpy(O).to(dev),
-                            G=Gd, U=U, I_host=I if keep else None, G_host=G if keep else None))
+                            G=Gd, U=U, I_host=I if keep else None, G_host=G if keep else None,
+                            A=None if A is None else torch.from_numpy(A).to(dev),
+                            A_host=A if keep else None))
     log(f"[bench] {args.batches} batches generated in {time.time() - t0:.1f}s; "
         f"U = {[x['U'] for x in batches]}")
 
@@ -336,6 +362,9 @@ def main():
     ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8, device=dev)
 
     def fwd(bt):
+        if pooled:
+            return pk.embbag_forward_pooled(tables, B, bt["I"], bt["O"], Y, bt["A"], pool_code,
+                                            status)
         if act_bf16:
             return pk.embbag_forward_split_bf16_act(hi, B, bt["I"], bt["O"], Y, status)
         if split:
@@ -343,9 +372,15 @@ def main():
         return pk.embbag_forward(tables, B, bt["I"], bt["O"], Y, status)
 
     def prep(bt):
+        if pooled:
+            return pk.embbag_backward_prepare_pooled(cfg.rows, E, B, bt["I"], bt["O"], ws, bt["A"],
+                                                     pool_code, status)
         return pk.embbag_backward_prepare(cfg.rows, E, B, bt["I"], bt["O"], ws, status)
 
     def apply(bt):
+        if pooled:
+            return pk.embbag_backward_apply_sgd_pooled(bt["G"], B, bt["O"], NS, cfg.lr, tables, ws,
+                                                       bt["A"], pool_code)
         if act_bf16:
             return pk.embbag_backward_apply_sgd_split_bf16_act(bt["G"], B, NS, cfg.lr, hi, lo, ws)
         if split:
@@ -405,7 +440,7 @@ def main():
     # per-step times: consecutive steps partition the timed region
     per_step = [(start if i == 0 else ev[i - 1][5]).elapsed_time(ev[i][5]) for i in range(K)]
     U_avg = sum(batches[i % len(batches)]["U"] for i in range(K)) / K
-    fwd_b, bwd_b = bytes_model(cfg, U_avg, split, act_bf16)
+    fwd_b, bwd_b = bytes_model(cfg, U_avg, split, act_bf16, args.pooling == "weighted")
     step_b = fwd_b + bwd_b
     gbps = step_b / (ms_step * 1e-3) / 1e9
     # B_min: the forward counted with one read per touched row instead of one per look-up
@@ -420,7 +455,7 @@ def main():
     # and one write of every touched row (2*U*E*4).
     TB = T * B
     sy = 2 if act_bf16 else 4
-    apply_b = sy * TB * E + 8 * NS + 2 * U_avg * E * 4
+    apply_b = sy * TB * E + 8 * NS + 2 * U_avg * E * 4 + (4 * NS if args.pooling == "weighted" else 0)
     if apply_ms >= fwd_ms:
         roof_call, roof_k, roof_b, roof_ms = ("apply", "segment_sgd+carry_group+segment_fixup",
                                               apply_b, apply_ms)
@@ -429,7 +464,7 @@ def main():
     achieved = roof_b / (roof_ms * 1e-3) / 1e9
     roof = {"kernel": roof_k, "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": profiled_traffic(workload_tag(cfg, act_bf16), roof_call),
+            "traffic": profiled_traffic(workload_tag(cfg, act_bf16, args.pooling), roof_call),
             "bytes_per_launch": int(roof_b),
             "avg_launch_ms": round(roof_ms, 4)}
 
@@ -446,7 +481,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": describe(cfg, act_bf16), "tables": T, "dim": E, "batch": B,
+        "config": {"workload": describe(cfg, act_bf16, args.pooling), "tables": T, "dim": E,
+                   "batch": B,
                    "pooling": cfg.pooling, "num_indices": NS, "unique_rows": round(U_avg),
                    "lr": cfg.lr, "batches_rotated": args.batches,
                    "streams": 2 if args.overlap_prepare else 1},
@@ -468,8 +504,10 @@ def main():
     if args.baselines and not split:
         out["baselines"] = time_baselines(pk, torch, cfg, tables, batches, main)
     if not args.no_cpu_baseline:
-        host = [(bt["I_host"], bt["G_host"]) for bt in batches if bt["I_host"] is not None]
-        out["cpu_baseline"] = cpu_baseline(cfg, host, args.cpu_sample_bags, act_bf16)
+        host = [(bt["I_host"], bt["G_host"], bt["A_host"]) for bt in batches
+                if bt["I_host"] is not None]
+        out["cpu_baseline"] = cpu_baseline(cfg, host, args.cpu_sample_bags, act_bf16,
+                                           args.pooling)
     print(json.dumps(out), flush=True)
 
 

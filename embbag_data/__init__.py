@@ -16,6 +16,7 @@ from .generators import (
     fill_tables_torch,
     make_batch,
     make_grads,
+    make_weights,
     random_bags,
     zipf_cdf,
     row_bijection,
@@ -25,6 +26,7 @@ from .generators import (
 __all__ = [
     "BASE_SEED", "Config", "get_config", "CONFIG_NAMES", "scaled",
     "splitmix64_np", "table_values_np", "table_values_torch", "table_rows_torch",
-    "fill_table_torch", "fill_tables_torch", "make_batch", "make_grads", "random_bags",
+    "fill_table_torch", "fill_tables_torch", "make_batch", "make_grads", "make_weights",
+    "random_bags",
     "zipf_cdf", "row_bijection", "mlperf_rows",
 ]

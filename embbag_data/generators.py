@@ -210,6 +210,17 @@ def make_grads(cfg, batch_id: int = 0) -> np.ndarray:
     return out
 
 
+def make_weights(cfg, batch_id: int = 0) -> np.ndarray:
+    """Per-look-up weights a_s (Section II's non-zero entries of A), U(0.5, 1.5)
+    FP32, one per look-up of make_batch's indices (table-major)."""
+    n_t = cfg.batch * cfg.pooling
+    out = np.empty(cfg.num_tables * n_t, dtype=np.float32)
+    for t in range(cfg.num_tables):
+        u = _table_rng(cfg, 3, batch_id, t).random(n_t, dtype=np.float32)
+        out[t * n_t:(t + 1) * n_t] = u + np.float32(0.5)
+    return out
+
+
 def random_bags(rng: np.random.Generator, rows, batch: int, max_pool: int,
                 empty_frac: float = 0.1, hot_frac: float = 0.0):
     """Variable-size bags for edge-case tests.

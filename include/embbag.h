@@ -139,6 +139,24 @@ int embbag_backward_sgd_pooled(const float* grad_pooled, int32_t batch, const in
                                const embbag_tables_t* tables, void* workspace,
                                size_t workspace_bytes, int32_t* d_status, hipStream_t stream);
 
+/* The same in two phases, like embbag_backward_prepare / _apply_sgd.  Phase 1
+ * sorts the weights, if given, along with the look-ups into the workspace
+ * (mean pooling needs nothing more than a plain phase 1); phase 2 must get the
+ * same (weights, pooling) pair, the same offsets (mean pooling reads the bag
+ * sizes from them) and the same sizes.  A workspace prepared with weights and
+ * applied without (or the reverse), or prepared for other sizes, makes the
+ * apply write nothing. */
+int embbag_backward_prepare_pooled(int32_t num_tables, const int64_t* rows, int32_t dim,
+                                   int32_t batch, const int32_t* indices, const int32_t* offsets,
+                                   int64_t num_indices, const float* per_sample_weights,
+                                   int32_t pooling, void* workspace, size_t workspace_bytes,
+                                   int32_t* d_status, hipStream_t stream);
+int embbag_backward_apply_sgd_pooled(const float* grad_pooled, int32_t batch,
+                                     const int32_t* offsets, int64_t num_indices,
+                                     const float* per_sample_weights, int32_t pooling, float lr,
+                                     const embbag_tables_t* tables, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
 /* The fused backward in two phases, for callers that overlap its integer
  * work with other parts of a training step.  embbag_backward_sgd(...) is
  * exactly embbag_backward_prepare(...) followed by embbag_backward_apply_sgd(...).

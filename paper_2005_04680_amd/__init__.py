@@ -69,6 +69,10 @@ def lib():
         L.embbag_backward_sgd_pooled.argtypes = [p, i32, p, p, i64, p, i32, C.c_float, p, p, sz,
                                                  p, p]
         L.embbag_backward_prepare.argtypes = [i32, p, i32, i32, p, p, i64, p, sz, p, p]
+        L.embbag_backward_prepare_pooled.argtypes = [i32, p, i32, i32, p, p, i64, p, i32, p, sz,
+                                                     p, p]
+        L.embbag_backward_apply_sgd_pooled.argtypes = [p, i32, p, i64, p, i32, C.c_float, p, p,
+                                                       sz, p]
         L.embbag_backward_apply_sgd.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
         L.embbag_backward_apply_sgd_split_bf16.argtypes = [p, i32, i64, C.c_float, p, p, sz, p]
         L.embbag_forward_split_bf16_act.argtypes = [p, i32, p, p, i64, p, p, p]
@@ -88,6 +92,7 @@ def lib():
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
                   "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
                   "embbag_forward_pooled", "embbag_backward_sgd_pooled",
+                  "embbag_backward_prepare_pooled", "embbag_backward_apply_sgd_pooled",
                   "embbag_backward_apply_sgd", "embbag_backward_apply_sgd_split_bf16",
                   "embbag_forward_split_bf16_act", "embbag_backward_sgd_split_bf16_act",
                   "embbag_backward_apply_sgd_split_bf16_act",
@@ -201,6 +206,31 @@ def embbag_backward_sgd_pooled(grad_pooled, batch, indices, offsets, lr, weights
         int(pooling), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
         int(workspace.numel() * workspace.element_size()), _ptr(d_status, _dt(*_I32), "d_status"),
         _stream(stream))
+
+
+def embbag_backward_prepare_pooled(rows, dim, batch, indices, offsets, workspace,
+                                   per_sample_weights=None, pooling=EMBBAG_POOL_SUM,
+                                   d_status=None, stream=None) -> int:
+    T = len(rows)
+    r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
+    return lib().embbag_backward_prepare_pooled(
+        T, C.cast(r, C.c_void_p), int(dim), int(batch), _ptr(indices, _dt(*_I32), "indices"),
+        _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
+        _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"), int(pooling),
+        _ptr(workspace, None, "workspace"), int(workspace.numel() * workspace.element_size()),
+        _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+
+
+def embbag_backward_apply_sgd_pooled(grad_pooled, batch, offsets, num_indices, lr, weights,
+                                     workspace, per_sample_weights=None,
+                                     pooling=EMBBAG_POOL_SUM, stream=None) -> int:
+    s, keep = _tables_struct(weights)
+    return lib().embbag_backward_apply_sgd_pooled(
+        _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
+        _ptr(offsets, _dt(*_I32), "offsets"), int(num_indices),
+        _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"), int(pooling), float(lr),
+        C.byref(s), _ptr(workspace, None, "workspace"),
+        int(workspace.numel() * workspace.element_size()), _stream(stream))
 
 
 def embbag_forward_split_bf16(hi, batch, indices, offsets, pooled_out, d_status=None,

@@ -75,16 +75,19 @@ int forward_common(const TableDesc& d, bool split, int32_t B, const int32_t* I, 
   return hip_status(launch_forward(d, split, B, I, O, NS, Y, y_bf16, d_status, pool, st));
 }
 
+// `weights` (weighted bags only) are sorted along with the look-ups.
 int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O, int64_t NS,
-                   void* ws, size_t ws_bytes, int32_t* d_status, int mode, hipStream_t st) {
+                   void* ws, size_t ws_bytes, int32_t* d_status, int mode, const float* weights,
+                   hipStream_t st) {
   int rc = check_bags(d.num_tables, B, I, O, NS);
   if (rc) return rc;
+  if (mode == kPoolWeighted && NS > 0 && weights == nullptr) return EMBBAG_ERR_INVALID_ARG;
   const uint32_t total = d.rowbase[d.num_tables];
   const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
   if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
   return hip_status(launch_sort(d, B, I, O, NS, L, static_cast<char*>(ws), d_status,
                                 phase_token(d.num_tables, B, NS, total, mode),
-                                mode == kPoolWeighted, st));
+                                mode == kPoolWeighted ? weights : nullptr, st));
 }
 
 int apply_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16, int32_t B,
@@ -109,7 +112,7 @@ int backward_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16
   if (rc) return rc;
   if (NS > 0 && (dY == nullptr || !aligned(dY, dy_bf16 ? 8 : 16))) return EMBBAG_ERR_INVALID_ARG;
   if (pool.mode == kPoolWeighted && NS > 0 && pool.weights == nullptr) return EMBBAG_ERR_INVALID_ARG;
-  rc = prepare_common(d, B, I, O, NS, ws, ws_bytes, d_status, pool.mode, st);
+  rc = prepare_common(d, B, I, O, NS, ws, ws_bytes, d_status, pool.mode, pool.weights, st);
   if (rc) return rc;
   return apply_common(d, split, dY, dy_bf16, B, NS, lr, ws, ws_bytes, pool, st);
 }
@@ -127,7 +130,7 @@ int split_desc(const embbag_split_tables_t* tables, bool need_lo, TableDesc* d) 
 namespace embbag {
 
 uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows, int mode) {
-  // The weighted payload (look-up positions) differs from the others (bags).
+  // A weighted prepare also sorts the weights along; the others do not.
   const uint64_t payload = mode == kPoolWeighted ? 1u : 0u;
   uint64_t h = 0x243F6A8885A308D3ull;
   for (uint64_t v : {uint64_t(uint32_t(T)), uint64_t(uint32_t(B)), uint64_t(NS),
@@ -186,7 +189,8 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   L.off_flags = take(64);
   L.off_carry = take(for_dedup ? 0 : size_t(2) * size_t(L.nchunks) * size_t(E) * 8);
   L.off_uniq = take(for_dedup ? size_t(L.ntiles) * 4 : 0);
-  L.off_bagof = take(for_dedup ? 0 : size_t(NS) * 4);
+  L.off_va = take(for_dedup ? 0 : size_t(NS) * 4);
+  L.off_vb = take(for_dedup ? 0 : size_t(NS) * 4);
   L.ngroups = (L.nchunks + kCarryGroup - 1) / kCarryGroup;
   L.off_gsum = take(for_dedup ? 0 : size_t(L.ngroups) * size_t(E) * 8);
   L.off_gflag = take(for_dedup ? 0 : size_t(L.ngroups) * 4);
@@ -296,6 +300,41 @@ int embbag_backward_sgd_pooled(const float* grad_pooled, int32_t batch, const in
                          workspace, workspace_bytes, d_status, pool, stream);
 }
 
+int embbag_backward_prepare_pooled(int32_t num_tables, const int64_t* rows, int32_t dim,
+                                   int32_t batch, const int32_t* indices, const int32_t* offsets,
+                                   int64_t num_indices, const float* per_sample_weights,
+                                   int32_t pooling, void* workspace, size_t workspace_bytes,
+                                   int32_t* d_status, hipStream_t stream) {
+  const int mode = pool_mode(per_sample_weights, pooling);
+  if (mode < 0) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(num_tables, dim, rows, nullptr, nullptr, 0, &d);
+  if (rc) return rc;
+  return prepare_common(d, batch, indices, offsets, num_indices, workspace, workspace_bytes,
+                        d_status, mode, per_sample_weights, stream);
+}
+
+int embbag_backward_apply_sgd_pooled(const float* grad_pooled, int32_t batch,
+                                     const int32_t* offsets, int64_t num_indices,
+                                     const float* per_sample_weights, int32_t pooling, float lr,
+                                     const embbag_tables_t* tables, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  const int mode = pool_mode(per_sample_weights, pooling);
+  if (mode < 0) return EMBBAG_ERR_INVALID_ARG;
+  if (mode == kPoolMean && num_indices > 0 && offsets == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  PoolArgs pool;
+  pool.mode = mode;
+  pool.weights = per_sample_weights;
+  pool.offsets = offsets;
+  return apply_common(d, false, grad_pooled, false, batch, num_indices, lr, workspace,
+                      workspace_bytes, pool, stream);
+}
+
 int embbag_backward_sgd_split_bf16(const float* grad_pooled, int32_t batch,
                                    const int32_t* indices, const int32_t* offsets,
                                    int64_t num_indices, float lr,
@@ -320,7 +359,7 @@ int embbag_backward_prepare(int32_t num_tables, const int64_t* rows, int32_t dim
   int rc = make_desc(num_tables, dim, rows, nullptr, nullptr, 0, &d);
   if (rc) return rc;
   return prepare_common(d, batch, indices, offsets, num_indices, workspace, workspace_bytes,
-                        d_status, kPoolPlain, stream);
+                        d_status, kPoolPlain, nullptr, stream);
 }
 
 int embbag_backward_apply_sgd(const float* grad_pooled, int32_t batch, int64_t num_indices,
@@ -424,7 +463,7 @@ int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const i
   char* w = static_cast<char*>(workspace);
   if (launch_sort(d, batch, indices, offsets, num_indices, L, w, d_status,
                   phase_token(num_tables, batch, num_indices, d.rowbase[num_tables], kPoolPlain),
-                  false, stream) != hipSuccess)
+                  nullptr, stream) != hipSuccess)
     return EMBBAG_ERR_HIP;
   return hip_status(launch_unique(sorted_buffer(L, w), L, w, sorted_keys, sorted_bags,
                                   unique_keys, seg_off, d_num_unique, stream));

@@ -103,8 +103,8 @@ struct BwdLayout {
   int passes;          // radix passes
   int bits;            // digit width of every pass
   int64_t ngroups;     // groups of kCarryGroup chunks
-  size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, off_bagof,
-      off_gsum, off_gflag,
+  size_t off_a, off_b, off_hist, off_tot, off_parts, off_flags, off_carry, off_uniq, off_va,
+      off_vb, off_gsum, off_gflag,
       total;
 };
 
@@ -121,17 +121,23 @@ inline uint64_t* sorted_buffer(const BwdLayout& L, char* ws) {
   return reinterpret_cast<uint64_t*>(ws + (passes % 2 == 0 ? L.off_a : L.off_b));
 }
 
+// The per-look-up weights in sorted order (weighted bags), beside it.
+inline float* sorted_values(const BwdLayout& L, char* ws) {
+  const int passes = L.ns > 0 ? L.passes : 0;
+  return reinterpret_cast<float*>(ws + (passes % 2 == 0 ? L.off_va : L.off_vb));
+}
+
 // Y is FP32 [T*B][E], or (y_bf16, split tables only) BF16 bit patterns.
 hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32_t* I,
                           const int32_t* O, int64_t NS, void* Y, bool y_bf16, int32_t* status,
                           const PoolArgs& pool, hipStream_t st);
 
 // Builds keys, validates, sorts into sorted_buffer(L, ws); stamps `token`.
-// The payload of a sorted word is the bag, or (by_lookup) the look-up
-// position s, with bag[s] then kept in the workspace.
+// The payload of a sorted word is the bag; with per-look-up weights A, the
+// weights are sorted along into sorted_values(L, ws).
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       uint32_t token, bool by_lookup, hipStream_t st);
+                       uint32_t token, const float* A, hipStream_t st);
 
 // dY is FP32 [T*B][E], or (dy_bf16, split tables only) BF16 bit patterns.
 hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const void* dY,

@@ -123,26 +123,13 @@ __device__ __forceinline__ void store_carry(double* carry, int64_t slot, int E, 
 }
 
 // Look-up coefficients of the gradient sum (Section II's weights a_p): 1 for
-// plain sums, the look-up's weight for weighted sums (the sorted payload is
-// then the look-up position s, and bagof[s] its bag), 1/|bag| for means.
+// plain sums, the look-up's weight for weighted sums (the weights sorted
+// along with the look-ups, so read in sorted order), 1/|bag| for means.
 struct PoolDev {
-  const uint32_t* bagof;
-  const float* weights;
+  const float* svals;
   const int32_t* offsets;
 };
 
-template <int MODE>
-__device__ __forceinline__ uint32_t bag_at(uint64_t p, const PoolDev& pd) {
-  if constexpr (MODE == kPoolWeighted) return pd.bagof[bag_of(p)];
-  return bag_of(p);
-}
-
-template <int MODE>
-__device__ __forceinline__ double coef_at(uint64_t p, uint32_t bag, const PoolDev& pd) {
-  if constexpr (MODE == kPoolWeighted) return double(pd.weights[bag_of(p)]);
-  if constexpr (MODE == kPoolMean) return 1.0 / double(pd.offsets[bag + 1] - pd.offsets[bag]);
-  return 1.0;
-}
 
 template <int LPR, int CPL, class Rows, int MODE, bool GBF16>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
@@ -169,7 +156,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   const uint32_t knext = hi < NS ? key_of(sorted[hi]) : kNoKey;
   const uint64_t p0 = sorted[lo];
   uint32_t cur = key_of(p0);
-  int ct = table_of_bag(bag_at<MODE>(p0, pd), B, inv_b);
+  int ct = table_of_bag(bag_of(p0), B, inv_b);
   const bool first_open = kprev == cur;  // first segment began in an earlier chunk
   bool is_first = true;
 
@@ -198,26 +185,47 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   // (skipped when a look-up repeats the previous (key, bag) pair: its row is
   // still in registers) and the W rows of the segments that start among them
   // are all requested before the first of them is used.
+  // Weighted bags: each look-up's weight is loaded one group ahead, with its
+  // word (the weights were sorted along with the look-ups).
+  constexpr bool kW = MODE == kPoolWeighted;
   uint64_t pn[U];
+  float an[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) pn[u] = lo + u < hi ? sorted[lo + u] : 0ull;
+  if constexpr (kW) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) an[u] = lo + u < hi ? pd.svals[lo + u] : 0.f;
+  }
   uint64_t plast = p0;  // look-up before the current group (none before lo: p0 itself)
   for (int s = lo; s < hi; s += U) {
     uint64_t p[U];
     uint32_t bg[U];
+    float aw[U];
+    int32_t ob0[U], ob1[U];
     bool dup[U], nseg[U];
     typename Dy<GBF16>::Raw g[U][CPL];
     typename Rows::Pre wp[U][CPL];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       p[u] = pn[u];
+      if constexpr (kW) aw[u] = an[u];
+      bg[u] = s + u < hi ? bag_of(p[u]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
       const uint64_t pq = u == 0 ? plast : p[u - 1];
       const bool valid = s + u < hi;
+      // a repeat of the previous look-up's (key, bag): its dY row is reused
       dup[u] = valid && p[u] == pq && !(s == lo && u == 0);
       nseg[u] = valid && key_of(p[u]) != key_of(pq);
     }
+    if constexpr (MODE == kPoolMean) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) bg[u] = s + u < hi ? bag_at<MODE>(p[u], pd) : 0u;
+      for (int u = 0; u < U; ++u) {
+        ob0[u] = s + u < hi ? pd.offsets[bg[u]] : 0;
+        ob1[u] = s + u < hi ? pd.offsets[bg[u] + 1] : 1;
+      }
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool ld = s + u < hi && !dup[u];
@@ -238,6 +246,10 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) pn[u] = s + U + u < hi ? sorted[s + U + u] : 0ull;
+    if constexpr (kW) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) an[u] = s + U + u < hi ? pd.svals[s + U + u] : 0.f;
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s + u >= hi) break;
@@ -256,7 +268,8 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
         }
       }
       double c = 1.0;
-      if constexpr (MODE != kPoolPlain) c = coef_at<MODE>(p[u], bg[u], pd);
+      if constexpr (kW) c = double(aw[u]);
+      if constexpr (MODE == kPoolMean) c = 1.0 / double(ob1[u] - ob0[u]);
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         if (!dup[u]) glast[j] = Dy<GBF16>::value(g[u][j]);
@@ -344,7 +357,7 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   if (key_of(sorted[hi]) != kl) return;             // last segment ends here
   const uint32_t kf = key_of(sorted[lo]);
   if (kf == kl && lo > 0 && key_of(sorted[lo - 1]) == kl) return;  // began earlier
-  const int ct = table_of_bag(bag_at<MODE>(sorted[hi - 1], pd), B, inv_b);
+  const int ct = table_of_bag(bag_of(sorted[hi - 1]), B, inv_b);
   const uint32_t r = kl - d.rowbase[ct];
   const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
 
@@ -518,7 +531,7 @@ hipError_t launch_segment_sgd(const TableDesc& d, bool split, int32_t B, const v
                               bool dy_bf16, float lr, const BwdLayout& L, char* ws,
                               uint32_t token, const PoolArgs& pool, hipStream_t st) {
   if (L.ns == 0) return hipSuccess;
-  PoolDev pd{reinterpret_cast<const uint32_t*>(ws + L.off_bagof), pool.weights, pool.offsets};
+  PoolDev pd{sorted_values(L, ws), pool.offsets};
   bool ok;
   if (split && dy_bf16)
     ok = launch_apply<SplitRows, kPoolPlain, true>(d, B, dY, lr, L, ws, token, pd, st);

@@ -59,12 +59,14 @@ struct Radix {
 };
 
 // Bags, keys and the first digit's histogram for one tile; offsets checks for
-// a slice of the bags; one status word per block.
+// a slice of the bags; one status word per block.  With per-look-up weights
+// A, vals[s] = A[s] starts the value array that the sort carries along.
 template <int BITS, int IPT>
 __global__ __launch_bounds__(kBlock) void build_keys(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, float inv_b, int32_t TB, int32_t ntiles, int32_t vb, uint64_t* __restrict__ out,
-    uint32_t* __restrict__ hist, int32_t* __restrict__ parts, uint32_t* __restrict__ bagof) {
+    uint32_t* __restrict__ hist, int32_t* __restrict__ parts, const float* __restrict__ A,
+    float* __restrict__ vals) {
   constexpr int R = Radix<BITS>::R;
   constexpr int TILE = kBlock * IPT;
   __shared__ uint32_t lbag[TILE];
@@ -121,12 +123,8 @@ __global__ __launch_bounds__(kBlock) void build_keys(
           r = 0;
         }
         key = d.rowbase[t] + uint32_t(r);
-        if (bagof != nullptr) {  // payload = look-up position, bag kept aside
-          out[s] = (uint64_t(key) << 32) | uint32_t(s);
-          bagof[s] = k;
-        } else {
-          out[s] = (uint64_t(key) << 32) | k;
-        }
+        out[s] = (uint64_t(key) << 32) | k;
+        if (A != nullptr) vals[s] = A[s];
       }
       if (s < s_hi) atomicAdd(&lhist[key & (R - 1)], 1u);
     }
@@ -198,15 +196,18 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
   if (tid == 0) totals[blockIdx.x] = running;
 }
 
-// Stable scatter of one tile by the digit at `shift`.
-template <int BITS, int IPT>
+// Stable scatter of one tile by the digit at `shift` (with VALS, the value
+// of each key moves with it: vsrc[i] goes where src[i] goes).
+template <int BITS, int IPT, bool VALS>
 __global__ __launch_bounds__(kBlock) void radix_downsweep(
     const uint64_t* __restrict__ src, uint64_t* __restrict__ dst, int32_t NS, int shift,
-    int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals) {
+    int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals,
+    const float* __restrict__ vsrc, float* __restrict__ vdst) {
   constexpr int R = Radix<BITS>::R;
   constexpr int DPT = Radix<BITS>::DPT;
   constexpr int TILE = kBlock * IPT;
   __shared__ uint64_t buf[TILE];
+  __shared__ float vbuf[VALS ? TILE : 1];
   __shared__ uint32_t whist[kWavesPerBlock][R];
   __shared__ uint32_t lstart[R];
   __shared__ uint32_t gbase[R];
@@ -241,12 +242,14 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   // being key w*64*IPT + i*64 + l: ranking item by item keeps the original order.
   const int wbase = blk * TILE + w * (kWave * IPT);
   uint64_t item[IPT];
+  float val[VALS ? IPT : 1];
   uint32_t dig[IPT];
   uint32_t rank[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
     const int pos = wbase + i * kWave + lane;
     item[i] = pos < NS ? src[pos] : ~0ull;
+    if constexpr (VALS) val[i] = pos < NS ? vsrc[pos] : 0.f;
   }
   const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
@@ -299,14 +302,20 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    if (wbase + i * kWave + lane < NS) buf[lstart[dig[i]] + whist[w][dig[i]] + rank[i]] = item[i];
+    if (wbase + i * kWave + lane < NS) {
+      const uint32_t at = lstart[dig[i]] + whist[w][dig[i]] + rank[i];
+      buf[at] = item[i];
+      if constexpr (VALS) vbuf[at] = val[i];
+    }
   }
   __syncthreads();
   const int nvalid = min(TILE, NS - blk * TILE);
   for (int j = tid; j < nvalid; j += kBlock) {
     const uint64_t it = buf[j];
     const uint32_t dg = (key_of(it) >> shift) & (R - 1);
-    dst[gbase[dg] + (j - lstart[dg])] = it;
+    const uint32_t to = gbase[dg] + (j - lstart[dg]);
+    dst[to] = it;
+    if constexpr (VALS) vdst[to] = vbuf[j];
   }
 }
 
@@ -388,7 +397,7 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
 template <int BITS, int IPT>
 hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       uint32_t token, bool by_lookup, hipStream_t st) {
+                       uint32_t token, const float* A, hipStream_t st) {
   constexpr int R = Radix<BITS>::R;
   const int32_t TB = d.num_tables * B;
   uint64_t* a = reinterpret_cast<uint64_t*>(ws + L.off_a);
@@ -401,9 +410,10 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   const int vb = (TB + 1 + nkb - 1) / nkb;
   const int ntiles = int(L.ntiles);
   const float inv_b = B > 0 ? 1.0f / float(B) : 0.0f;
-  uint32_t* bagof = by_lookup ? reinterpret_cast<uint32_t*>(ws + L.off_bagof) : nullptr;
-  hipLaunchKernelGGL((build_keys<BITS, IPT>), dim3(nkb), dim3(kBlock), 0, st, d, I, O, int32_t(NS), B,
-                     inv_b, TB, ntiles, vb, a, hist, parts, bagof);
+  float* va = reinterpret_cast<float*>(ws + L.off_va);
+  float* vb_ = reinterpret_cast<float*>(ws + L.off_vb);
+  hipLaunchKernelGGL((build_keys<BITS, IPT>), dim3(nkb), dim3(kBlock), 0, st, d, I, O,
+                     int32_t(NS), B, inv_b, TB, ntiles, vb, a, hist, parts, A, va);
   // Status verdict (block R of the first scan, or alone when nothing is sorted).
   const int passes = NS > 0 ? L.passes : 0;
   if (passes == 0) {
@@ -413,6 +423,8 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   }
   uint64_t* src = a;
   uint64_t* dst = b;
+  float* vsrc = va;
+  float* vdst = vb_;
   for (int p = 0; p < passes; ++p) {
     const int shift = p * BITS;
     if (p > 0)
@@ -420,11 +432,18 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
                          int32_t(NS), shift, ntiles, hist);
     hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? R + 1 : R), dim3(kBlock), 0, st, hist, ntiles, R,
                        totals, parts, nkb, flags, d_status, token);
-    hipLaunchKernelGGL((radix_downsweep<BITS, IPT>), dim3(ntiles), dim3(kBlock), 0, st, src, dst,
-                       int32_t(NS), shift, ntiles, hist, totals);
+    if (A != nullptr)
+      hipLaunchKernelGGL((radix_downsweep<BITS, IPT, true>), dim3(ntiles), dim3(kBlock), 0, st,
+                         src, dst, int32_t(NS), shift, ntiles, hist, totals, vsrc, vdst);
+    else
+      hipLaunchKernelGGL((radix_downsweep<BITS, IPT, false>), dim3(ntiles), dim3(kBlock), 0, st,
+                         src, dst, int32_t(NS), shift, ntiles, hist, totals, nullptr, nullptr);
     uint64_t* tmp = src;
     src = dst;
     dst = tmp;
+    float* vt = vsrc;
+    vsrc = vdst;
+    vdst = vt;
   }
   return hipGetLastError();
 }
@@ -432,11 +451,11 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
 template <int BITS>
 hipError_t sort_ipt(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O, int64_t NS,
                     const BwdLayout& L, char* ws, int32_t* d_status, uint32_t token,
-                    bool by_lookup, hipStream_t st) {
+                    const float* A, hipStream_t st) {
   switch (L.ipt) {
-    case 4: return sort_passes<BITS, 4>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 8: return sort_passes<BITS, 8>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 16: return sort_passes<BITS, 16>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 4: return sort_passes<BITS, 4>(d, B, I, O, NS, L, ws, d_status, token, A, st);
+    case 8: return sort_passes<BITS, 8>(d, B, I, O, NS, L, ws, d_status, token, A, st);
+    case 16: return sort_passes<BITS, 16>(d, B, I, O, NS, L, ws, d_status, token, A, st);
   }
   return hipErrorInvalidValue;
 }
@@ -458,13 +477,13 @@ void unique_launch(const uint64_t* sorted, const BwdLayout& L, uint32_t* counts,
 
 hipError_t launch_sort(const TableDesc& d, int32_t B, const int32_t* I, const int32_t* O,
                        int64_t NS, const BwdLayout& L, char* ws, int32_t* d_status,
-                       uint32_t token, bool by_lookup, hipStream_t st) {
+                       uint32_t token, const float* A, hipStream_t st) {
   switch (L.bits) {
-    case 6: return sort_ipt<6>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 7: return sort_ipt<7>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 8: return sort_ipt<8>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 9: return sort_ipt<9>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
-    case 10: return sort_ipt<10>(d, B, I, O, NS, L, ws, d_status, token, by_lookup, st);
+    case 6: return sort_ipt<6>(d, B, I, O, NS, L, ws, d_status, token, A, st);
+    case 7: return sort_ipt<7>(d, B, I, O, NS, L, ws, d_status, token, A, st);
+    case 8: return sort_ipt<8>(d, B, I, O, NS, L, ws, d_status, token, A, st);
+    case 9: return sort_ipt<9>(d, B, I, O, NS, L, ws, d_status, token, A, st);
+    case 10: return sort_ipt<10>(d, B, I, O, NS, L, ws, d_status, token, A, st);
   }
   return hipErrorInvalidValue;
 }

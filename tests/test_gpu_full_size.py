@@ -19,7 +19,7 @@ import torch
 import oracle
 import paper_2005_04680_amd as pk
 from embbag_data import (fill_table_torch, fill_tables_torch, get_config, make_batch, make_grads,
-                         table_rows_torch, table_values_np)
+                         make_weights, table_rows_torch, table_values_np)
 from gpu_util import (DEV, assert_bf16_bracket, assert_close, bf16_bits, bits_equal, gpu_dedup, log,
                       require_gpu, to_bf16_bits)
 
@@ -190,6 +190,66 @@ def _run_split(name, grad_bf16):
         assert bits_equal(got[t][0][is_u], hi_c[t][is_u]), f"{name} table {t} untouched hi changed"
         assert bits_equal(got[t][1][is_u], lo_c[t][is_u]), f"{name} table {t} untouched lo changed"
     log(f"[full] {name}: ok")
+
+
+def _run_pooled(name, pooling):
+    """Weighted-sum or mean pooling (f1) at full size, as bench.py --pooling runs it."""
+    cfg = get_config(name)
+    T, B, E, P, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.pooling, cfg.num_indices
+    log(f"[full] {name} {pooling}: filling {cfg.table_bytes / 1e9:.1f} GB on the device")
+    W = [torch.empty((m, E), dtype=torch.float32, device=DEV) for m in cfg.rows]
+    fill_tables_torch(cfg, W)
+    I, O = make_batch(cfg, 0, device=DEV)
+    G = make_grads(cfg, 0)
+    a = make_weights(cfg, 0) if pooling == "weighted" else None
+    pool = pk.EMBBAG_POOL_MEAN if pooling == "mean" else pk.EMBBAG_POOL_SUM
+    om = oracle.POOL_MEAN if pooling == "mean" else oracle.POOL_SUM
+    rng = np.random.default_rng(9)
+    sel, I_c, untouched = [], np.empty_like(I), []
+    for t in range(T):
+        lo, hi = t * B * P, (t + 1) * B * P
+        touched = np.unique(I[lo:hi])
+        cand = rng.integers(0, cfg.rows[t], 2000)
+        cand = np.setdiff1d(np.unique(cand), touched)[: max(1, 10000 // T)]
+        rows = np.union1d(touched, cand)
+        I_c[lo:hi] = np.searchsorted(rows, I[lo:hi])
+        sel.append(rows)
+        untouched.append(cand)
+    W_c = [table_rows_torch(cfg.seed, t, torch.from_numpy(sel[t]).to(DEV), E,
+                            cfg.value_scale[t]).cpu().numpy() for t in range(T)]
+    log(f"[full] {name} {pooling}: GPU forward + backward")
+    Id, Od, Gd = (torch.from_numpy(x).to(DEV) for x in (I, O, G))
+    ad = None if a is None else torch.from_numpy(a).to(DEV)
+    Y = torch.empty((T, B, E), dtype=torch.float32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8, device=DEV)
+    assert pk.embbag_forward_pooled(W, B, Id, Od, Y, ad, pool, status) == 0
+    assert pk.embbag_backward_prepare_pooled(cfg.rows, E, B, Id, Od, ws, ad, pool, status) == 0
+    assert pk.embbag_backward_apply_sgd_pooled(Gd, B, Od, NS, cfg.lr, W, ws, ad, pool) == 0
+    assert pk.embbag_status_read(status) == 0
+    Y = Y.cpu().numpy()
+    W_gpu = [W[t][torch.from_numpy(sel[t]).to(DEV)].cpu().numpy() for t in range(T)]
+    del W
+    torch.cuda.empty_cache()
+    log(f"[full] {name} {pooling}: oracle")
+    rc, Y_ref = oracle.forward_weighted(W_c, B, I_c, O, a, om)
+    assert rc == 0
+    assert_close(Y, Y_ref, f"{name} {pooling} pooled")
+    W_ref = [w.copy() for w in W_c]
+    assert oracle.backward_sgd_weighted(G, B, I_c, O, cfg.lr, W_ref, a, om) == 0
+    for t in range(T):
+        is_u = np.isin(sel[t], untouched[t])
+        assert_close(W_gpu[t][~is_u], W_ref[t][~is_u], f"{name} {pooling} table {t} touched rows")
+        assert bits_equal(W_gpu[t][is_u], W_c[t][is_u]), f"{name} table {t} untouched rows changed"
+    log(f"[full] {name} {pooling}: ok")
+
+
+def test_large_weighted_full_size():
+    _run_pooled("large", "weighted")
+
+
+def test_large_mean_full_size():
+    _run_pooled("large", "mean")
 
 
 def test_large_full_size():

@@ -532,16 +532,31 @@ def test_weighted_and_mean(dim, mode, maxp):
     assert_close(Y.cpu().numpy(), Yref, f"{mode} pooled")
     ws = torch.empty(pk.embbag_backward_workspace_bytes(len(rows), batch, I.size, dim),
                      dtype=torch.uint8, device=DEV)
+    two = GpuTables(W)  # the same update in two phases
     assert pk.embbag_backward_sgd_pooled(Gd, batch, Id, Od, 0.1, gt.w, ws, ad, pool, gt.status) == 0
     assert gt.read_status() == 0
+    ws2 = torch.empty_like(ws)
+    assert pk.embbag_backward_prepare_pooled(rows, dim, batch, Id, Od, ws2, ad, pool,
+                                             two.status) == 0
+    assert pk.embbag_backward_apply_sgd_pooled(Gd, batch, Od, I.size, 0.1, two.w, ws2, ad,
+                                               pool) == 0
+    assert two.read_status() == 0
     Wref = [w.copy() for w in W]
     assert oracle.backward_sgd_weighted(G, batch, I, O, 0.1, Wref, a, om) == 0
-    for t, (wg, wr) in enumerate(zip(gt.host(), Wref)):
+    for t, (wg, wr, w2) in enumerate(zip(gt.host(), Wref, two.host())):
         assert_close(wg, wr, f"{mode} table {t}")
-    # a weighted workspace is not taken for a plain apply
+        assert bits_equal(w2, wg), f"{mode} table {t}: two-phase differs from fused"
+    # a weighted workspace is not taken for an unweighted apply, nor the reverse
     if mode == "weighted":
         before = gt.host()
         assert pk.embbag_backward_apply_sgd(Gd, batch, I.size, 0.1, gt.w, ws) == 0
+        assert pk.embbag_backward_apply_sgd_pooled(Gd, batch, Od, I.size, 0.1, gt.w, ws, None,
+                                                   pk.EMBBAG_POOL_MEAN) == 0
+        for x, y in zip(gt.host(), before):
+            assert bits_equal(x, y)
+        assert pk.embbag_backward_prepare(rows, dim, batch, Id, Od, ws, gt.status) == 0
+        assert pk.embbag_backward_apply_sgd_pooled(Gd, batch, Od, I.size, 0.1, gt.w, ws, ad,
+                                                   pool) == 0
         for x, y in zip(gt.host(), before):
             assert bits_equal(x, y)
 
