@@ -1,7 +1,11 @@
-"""The training step (backward prepare, forward, backward apply) captured as a
+"""Stream and graph use of the boundary.
+
+The training step (backward prepare, forward, backward apply) captured as a
 HIP graph and replayed: every replay must give, bit for bit, what the same
 calls give when launched directly (the kernels are deterministic).  Eager work
-and synchronisations run between the replays, and each replay is checked."""
+and synchronisations run between the replays, and each replay is checked.
+Two steps on two streams at once, each with its own buffers, must both match
+the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -101,3 +105,45 @@ def test_graph_replays_match_direct_launches(split):
                 assert torch.equal(la[t], lb[t]), f"replay {it}: lo half {t} differs"
         log(f"[graph] replay {it} ok")
     del g
+
+
+def test_two_streams_at_once():
+    """The library keeps no global state: two steps on two streams, each with
+    its own tables and workspace, overlap and both match the oracle."""
+    import oracle
+    from gpu_util import GpuTables, assert_close
+    from embbag_data import random_bags
+
+    def inputs(seed):
+        rng = np.random.default_rng(seed)
+        rows, E, B = (3000, 500, 2000), 64, 300
+        W = [rng.uniform(-0.05, 0.05, (m, E)).astype(np.float32) for m in rows]
+        I, O = random_bags(rng, rows, B, 20, 0.05, 0.3)
+        G = rng.standard_normal((len(rows), B, E)).astype(np.float32)
+        return rows, E, B, W, I, O, G
+
+    cases = [inputs(1), inputs(2)]
+    gts = [GpuTables(c[3]) for c in cases]
+    streams = [torch.cuda.Stream(device=DEV), torch.cuda.Stream(device=DEV)]
+    outs = []
+    torch.cuda.synchronize()
+    for (rows, E, B, W, I, O, G), gt, st in zip(cases, gts, streams):
+        with torch.cuda.stream(st):
+            Id, Od, Gd = (torch.from_numpy(a).to(DEV, non_blocking=False) for a in (I, O, G))
+            Y = torch.empty((len(rows), B, E), dtype=torch.float32, device=DEV)
+            ws = torch.empty(pk.embbag_backward_workspace_bytes(len(rows), B, I.size, E),
+                             dtype=torch.uint8, device=DEV)
+            for _ in range(3):  # several launches in flight on each stream
+                assert pk.embbag_forward(gt.w, B, Id, Od, Y, gt.status) == 0
+            assert pk.embbag_backward_sgd(Gd, B, Id, Od, 0.1, gt.w, ws, gt.status) == 0
+            outs.append((Y, Id, Od, Gd, ws))
+    torch.cuda.synchronize()
+    for (rows, E, B, W, I, O, G), gt, (Y, *_keep) in zip(cases, gts, outs):
+        assert gt.read_status() == 0
+        rc, Yref = oracle.forward(W, B, I, O)
+        assert rc == 0
+        assert_close(Y.cpu().numpy(), Yref, "pooled")
+        Wref = [w.copy() for w in W]
+        assert oracle.backward_sgd(G, B, I, O, 0.1, Wref) == 0
+        for t, (wg, wr) in enumerate(zip(gt.host(), Wref)):
+            assert_close(wg, wr, f"table {t}")
