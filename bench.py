@@ -124,7 +124,7 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
 
     P, B, T = cfg.pooling, cfg.batch, cfg.num_tables
     nb = min(sample_bags, B)
-    dt, n_look, n_rows = 0.0, 0, 0
+    dt, dt_f, dt_b, n_look, n_rows = 0.0, 0.0, 0.0, 0, 0
     # one host core for the whole timed region (the oracle is single-threaded)
     old_aff = os.sched_getaffinity(0)
     core = min(old_aff)
@@ -151,24 +151,27 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
         if cfg.split and act_bf16:
             Gb = np.ascontiguousarray(torch.from_numpy(G_s).to(torch.bfloat16).view(torch.int16)
                                       .numpy().view(np.uint16))
-            t0 = time.perf_counter()
-            rc1, _ = oracle.forward_split_bf16_act(his, nb, I_s, O_s)
-            rc2 = oracle.backward_sgd_split_bf16_act(Gb, nb, I_s, O_s, cfg.lr, his, los)
+            fwd = lambda: oracle.forward_split_bf16_act(his, nb, I_s, O_s)[0]
+            bwd = lambda: oracle.backward_sgd_split_bf16_act(Gb, nb, I_s, O_s, cfg.lr, his, los)
         elif cfg.split:
-            t0 = time.perf_counter()
-            rc1, _ = oracle.forward_split(his, nb, I_s, O_s)
-            rc2 = oracle.backward_sgd_split(G_s, nb, I_s, O_s, cfg.lr, his, los)
+            fwd = lambda: oracle.forward_split(his, nb, I_s, O_s)[0]
+            bwd = lambda: oracle.backward_sgd_split(G_s, nb, I_s, O_s, cfg.lr, his, los)
         elif pooling != "sum":
             mode = oracle.POOL_MEAN if pooling == "mean" else oracle.POOL_SUM
             a = np.ascontiguousarray(np.concatenate(A_s)) if A_s else None
-            t0 = time.perf_counter()
-            rc1, _ = oracle.forward_weighted(tabs, nb, I_s, O_s, a, mode)
-            rc2 = oracle.backward_sgd_weighted(G_s, nb, I_s, O_s, cfg.lr, tabs, a, mode)
+            fwd = lambda: oracle.forward_weighted(tabs, nb, I_s, O_s, a, mode)[0]
+            bwd = lambda: oracle.backward_sgd_weighted(G_s, nb, I_s, O_s, cfg.lr, tabs, a, mode)
         else:
-            t0 = time.perf_counter()
-            rc1, _ = oracle.forward(tabs, nb, I_s, O_s)
-            rc2 = oracle.backward_sgd(G_s, nb, I_s, O_s, cfg.lr, tabs)
-        dt += time.perf_counter() - t0
+            fwd = lambda: oracle.forward(tabs, nb, I_s, O_s)[0]
+            bwd = lambda: oracle.backward_sgd(G_s, nb, I_s, O_s, cfg.lr, tabs)
+        t0 = time.perf_counter()
+        rc1 = fwd()
+        t1 = time.perf_counter()
+        rc2 = bwd()
+        t2 = time.perf_counter()
+        dt_f += t1 - t0
+        dt_b += t2 - t1
+        dt += t2 - t0
         assert rc1 == 0 and rc2 == 0
         n_look += I_s.size
     os.sched_setaffinity(0, old_aff)
@@ -176,7 +179,9 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
             "sample": (f"first {nb} of {B} bags of each of the {T} tables of batches "
                        f"0-{len(host_batches) - 1} ({n_look} look-ups, {n_rows} touched rows), "
                        f"forward + fused backward/SGD, single-threaded, {dt:.2f} s"),
-            "host": host_cpu(), "core": core}
+            "host": host_cpu(), "core": core,
+            "forward_lookups_per_s": round(n_look / dt_f, 1),
+            "backward_sgd_lookups_per_s": round(n_look / dt_b, 1)}
 
 
 def time_graph(torch, batches, prep, fwd, apply, K, warmup):
