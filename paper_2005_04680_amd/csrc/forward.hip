@@ -31,6 +31,10 @@ __device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, int E, i
   }
 }
 
+__device__ __forceinline__ d4 to_d4(const f4& v) {
+  return d4{double(v.x), double(v.y), double(v.z), double(v.w)};
+}
+
 // FP32 -> BF16, round to nearest, ties to even (NaN stays a quiet NaN).
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
   const uint32_t b = __float_as_uint(f);
@@ -61,16 +65,18 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   const void* base = d.w[t];
   int err = 0;
 
-  // Stores bag k's pooled row; mean pooling divides by the bag's n look-ups.
-  // BF16 outputs are the FP32 sums rounded to nearest even.
-  auto store_bag = [&](int k, const f4* acc, int n) {
+  // Stores bag k's pooled row, the FP64 sum rounded once to FP32; mean
+  // pooling divides by the bag's n look-ups first.  BF16 outputs are the FP32
+  // values rounded to nearest even.
+  auto store_bag = [&](int k, const d4* acc, int n) {
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
       const int c4 = rl + j * LPR;
-      f4 v = acc[j];
+      d4 a = acc[j];
       if constexpr (MODE == kPoolMean) {
-        if (n > 0) v = v / float(n);
+        if (n > 0) a = a / double(n);
       }
+      const f4 v = f4{float(a.x), float(a.y), float(a.z), float(a.w)};
       if (c4 >= E4) continue;
       if constexpr (YBF16) {
         u2 h;
@@ -94,9 +100,9 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
     bad = bad || bound < s0 || bound > s1;
   }
 
-  f4 acc[CPL];
+  d4 acc[CPL];
 #pragma unroll
-  for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < CPL; ++j) acc[j] = d4{0.0, 0.0, 0.0, 0.0};
 
   // Indices arrive in windows of LPR look-ups, one per lane of the row group
   // (a coalesced load), the next window already in flight; each look-up's
@@ -171,7 +177,7 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
           store_bag(k, acc, bound - bstart);
           bstart = bound;
 #pragma unroll
-          for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+          for (int j = 0; j < CPL; ++j) acc[j] = d4{0.0, 0.0, 0.0, 0.0};
           ++k;
           const int nb = O[k + 1];
           if (nb < bound || nb > s1) {
@@ -185,9 +191,9 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         if constexpr (MODE == kPoolWeighted)
-          acc[j] = use[u] ? acc[j] + wt[u] * v[u][j] : acc[j];
+          acc[j] = use[u] ? acc[j] + double(wt[u]) * to_d4(v[u][j]) : acc[j];
         else
-          acc[j] = use[u] ? acc[j] + v[u][j] : acc[j];
+          acc[j] = use[u] ? acc[j] + to_d4(v[u][j]) : acc[j];
       }
     }
   }
@@ -198,7 +204,7 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
       for (int kk = k + 1; kk < k1; ++kk) {
         if (O[kk] != s1) bad = true;
 #pragma unroll
-        for (int j = 0; j < CPL; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < CPL; ++j) acc[j] = d4{0.0, 0.0, 0.0, 0.0};
         store_bag(kk, acc, 0);
       }
     }

@@ -1,0 +1,84 @@
+"""The Python binding on the CPU: it only marshals arguments, so it must refuse
+host tensors, non-contiguous tensors and wrong dtypes before any library call,
+fail loudly when the library is missing, and raise EmbbagError on a bad status.
+(No GPU here: nothing below reaches a HIP call.)"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2005_04680_amd as pk
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(pk, "LIB_PATH", str(tmp_path / "libembbag.so"))
+    monkeypatch.setattr(pk, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        pk.lib()
+
+
+def test_host_tensors_are_refused():
+    W = [torch.zeros((10, 8))]
+    I = torch.zeros(4, dtype=torch.int32)
+    O = torch.tensor([0, 4], dtype=torch.int32)
+    Y = torch.zeros((1, 1, 8))
+    with pytest.raises(TypeError, match="GPU tensor"):
+        pk.embbag_forward(W, 1, I, O, Y)
+    with pytest.raises(TypeError, match="GPU tensor"):
+        pk.embbag_backward_sgd(Y, 1, I, O, 0.1, W, torch.zeros(1024, dtype=torch.uint8))
+    with pytest.raises(TypeError, match="GPU tensor"):
+        pk.embbag_forward_split_bf16([torch.zeros((10, 8), dtype=torch.int16)], 1, I, O, Y)
+    with pytest.raises(TypeError, match="GPU tensor"):
+        pk.embbag_split_fp32(torch.zeros(8), torch.zeros(8, dtype=torch.int16),
+                             torch.zeros(8, dtype=torch.int16))
+
+
+def test_status_codes_and_check():
+    assert pk.embbag_status_string(pk.EMBBAG_OK) == "ok"
+    assert "index" in pk.embbag_status_string(pk.EMBBAG_ERR_INDEX_RANGE)
+    pk.check(pk.EMBBAG_OK)
+    with pytest.raises(pk.EmbbagError) as e:
+        pk.check(pk.EMBBAG_ERR_OFFSETS, "backward")
+    assert e.value.code == pk.EMBBAG_ERR_OFFSETS and "offsets" in str(e.value)
+
+
+def test_workspace_size_marshalling():
+    n = pk.embbag_backward_workspace_bytes(16, 8192, 16 * 8192 * 100, 256)
+    assert n > 16 * 8192 * 100 * 16  # two 64-bit key buffers at least
+    assert pk.embbag_backward_workspace_bytes(0, 8, 10, 16) == 0  # invalid table count
+    assert pk.embbag_dedup_workspace_bytes(4, 32, 512) > 0
+
+
+class _FakeCuda:
+    """Stands in for a GPU tensor so that the binding's dtype and layout checks
+    run on the CPU; its address is never dereferenced."""
+
+    def __init__(self, t):
+        self._t = t
+        self.is_cuda = True
+        self.dtype = t.dtype
+        self.shape = t.shape
+
+    def is_contiguous(self):
+        return self._t.is_contiguous()
+
+    def data_ptr(self):
+        return 4096  # a dummy address: the checks under test fail before any library call
+
+    def numel(self):
+        return self._t.numel()
+
+    def element_size(self):
+        return self._t.element_size()
+
+
+def test_dtype_and_layout_checks():
+    W = [_FakeCuda(torch.zeros((10, 8)))]
+    O = _FakeCuda(torch.zeros(2, dtype=torch.int32))
+    Y = _FakeCuda(torch.zeros((1, 1, 8)))
+    with pytest.raises(TypeError, match="indices"):
+        pk.embbag_forward(W, 1, _FakeCuda(torch.zeros(4, dtype=torch.int64)), O, Y)
+    with pytest.raises(TypeError, match="contiguous"):
+        pk.embbag_forward(W, 1, _FakeCuda(torch.zeros((4, 2), dtype=torch.int32).t()), O, Y)
+    with pytest.raises(TypeError, match="pooled_out"):
+        pk.embbag_forward_split_bf16_act([_FakeCuda(torch.zeros((10, 8), dtype=torch.int16))], 1,
+                                         _FakeCuda(torch.zeros(4, dtype=torch.int32)), O, Y)

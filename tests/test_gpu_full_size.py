@@ -82,6 +82,7 @@ def _run(name):
     rc, Y_ref = oracle.forward(W_c, B, I_c, O)
     assert rc == 0
     assert_close(Y, Y_ref, f"{name} pooled")
+    assert bits_equal(Y, Y_ref), f"{name}: pooled outputs not bit-identical"
     log(f"[full] {name}: oracle backward")
     W_ref = [w.copy() for w in W_c]
     assert oracle.backward_sgd(G, B, I_c, O, cfg.lr, W_ref) == 0
@@ -172,6 +173,7 @@ def _run_split(name, grad_bf16):
     rc, Y_ref = oracle.forward_split(hi_c, B, I_c, O)
     assert rc == 0
     assert_close(Y, Y_ref, f"{name} pooled")
+    assert bits_equal(Y, Y_ref), f"{name}: pooled outputs not bit-identical"
     ndiff = assert_bf16_bracket(Yb, Y_ref, f"{name} pooled bf16")
     log(f"[full] {name}: BF16 outputs differing from the rounded oracle value: {ndiff} of {Yb.size}")
     if P == 1:
@@ -235,6 +237,7 @@ def _run_pooled(name, pooling):
     rc, Y_ref = oracle.forward_weighted(W_c, B, I_c, O, a, om)
     assert rc == 0
     assert_close(Y, Y_ref, f"{name} {pooling} pooled")
+    assert bits_equal(Y, Y_ref), f"{name} {pooling}: pooled outputs not bit-identical"
     W_ref = [w.copy() for w in W_c]
     assert oracle.backward_sgd_weighted(G, B, I_c, O, cfg.lr, W_ref, a, om) == 0
     for t in range(T):
