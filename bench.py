@@ -223,6 +223,23 @@ def time_graph(torch, batches, prep, fwd, apply, K, warmup):
     return {"ms_per_step": round(ms, 4), "replays": K, "graphs": len(batches)}
 
 
+def time_floor(pk, torch, tables, bt, B, NS, prep, ws, stream, K):
+    """Mean ms of the update's floor on the rows of batch `bt`: every touched
+    row read and written back once (embbag_baseline_touch_rows, which leaves
+    the tables unchanged), K calls back to back on one prepared workspace
+    between two events on `stream`."""
+    pk.check(prep(bt), "prepare")
+    pk.check(pk.embbag_baseline_touch_rows(B, NS, tables, ws), "touch rows")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(K):
+        pk.check(pk.embbag_baseline_touch_rows(B, NS, tables, ws), "touch rows")
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / K
+
+
 def time_baselines(pk, torch, cfg, tables, batches, stream, reps=3):
     """Average ms per step of the unfused designs, same workload and stream."""
     T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
@@ -486,6 +503,14 @@ def main():
             "traffic": profiled_traffic(workload_tag(cfg, act_bf16, args.pooling), roof_call),
             "bytes_per_launch": int(roof_b),
             "avg_launch_ms": round(roof_ms, 4)}
+    if roof_call == "apply" and not split and not pooled:
+        # The apply's floor on this GPU: the read and write-back of the same
+        # touched rows with nothing summed (no gradient gathers).
+        # (the rows of batch 0; its U is within 0.2% of the average)
+        floor_ms = time_floor(pk, torch, tables, batches[0], B, NS, prep, ws, main, K)
+        roof["floor_ms"] = round(floor_ms, 4)
+        roof["floor_gbps"] = round(2 * batches[0]["U"] * E * 4 / (floor_ms * 1e-3) / 1e9, 1)
+        roof["frac_of_floor"] = round(floor_ms / roof_ms, 4)
 
     out = {
         "metric": METRIC,

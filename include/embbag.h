@@ -293,6 +293,17 @@ int embbag_baseline_update_owner(const float* dW, int32_t batch, const int32_t* 
                                  const embbag_tables_t* tables, int32_t owners,
                                  hipStream_t stream);
 
+/* The floor of the update, for measurement: every row that the workspace
+ * prepared by embbag_backward_prepare (same batch, num_indices and tables,
+ * no weights) touches is read and written back unchanged, once: the memory
+ * traffic of the single-writer update of Algorithm 4 with nothing summed.
+ * Its time bounds embbag_backward_apply_sgd on the same rows from below.
+ * Tables are left bit-identical.  A workspace that holds no sort result for
+ * these sizes (or a data error) makes it write nothing.  Argument errors as
+ * embbag_backward_apply_sgd. */
+int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_tables_t* tables,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Waits for `stream` and returns the device status word (*d_status), or
  * EMBBAG_ERR_HIP if the wait or copy fails. */
 int embbag_status_read(const int32_t* d_status, hipStream_t stream);

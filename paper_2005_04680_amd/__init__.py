@@ -88,6 +88,7 @@ def lib():
         L.embbag_baseline_update_atomic.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
         L.embbag_baseline_backward_sgd_atomic.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
         L.embbag_baseline_update_owner.argtypes = [p, i32, p, p, i64, C.c_float, p, i32, p]
+        L.embbag_baseline_touch_rows.argtypes = [i32, i64, p, p, sz, p]
         L.embbag_status_read.argtypes = [p, p]
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
                   "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
@@ -99,7 +100,7 @@ def lib():
                   "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
                   "embbag_baseline_materialize", "embbag_baseline_update_atomic",
                   "embbag_baseline_backward_sgd_atomic", "embbag_baseline_update_owner",
-                  "embbag_status_read"):
+                  "embbag_baseline_touch_rows", "embbag_status_read"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -413,6 +414,14 @@ def embbag_baseline_update_owner(dW, batch, indices, offsets, lr, weights, owner
                                               _ptr(offsets, _dt(*_I32), "offsets"),
                                               int(indices.numel()), float(lr), C.byref(s),
                                               int(owners), _stream(stream))
+
+
+def embbag_baseline_touch_rows(batch, num_indices, weights, workspace, stream=None) -> int:
+    s, keep = _tables_struct(weights)
+    return lib().embbag_baseline_touch_rows(int(batch), int(num_indices), C.byref(s),
+                                            _ptr(workspace, None, "workspace"),
+                                            int(workspace.numel() * workspace.element_size()),
+                                            _stream(stream))
 
 
 def embbag_status_read(d_status, stream=None) -> int:

@@ -11,6 +11,8 @@
 //     look-ups in order and applies those it owns, one at a time.
 // Atomics make the FP32 sum order scheduling-dependent; the owner update
 // applies each row's look-ups in increasing s, like a sequential loop.
+// A last kernel is no design of the paper but the floor of every update: the
+// read and write-back of each touched row, once, with nothing summed.
 #include "common.hpp"
 
 namespace embbag {
@@ -155,6 +157,65 @@ __global__ __launch_bounds__(kWave) void owner_update_kernel(TableDesc d,
   }
 }
 
+
+// The update's data movement alone: the look-ups sorted by a prepared
+// workspace are cut into the same chunks as the fused update's; a row group
+// walks its chunk H look-ups at a time, and for each segment that begins
+// there reads the row and writes it back unchanged (an SGD step with a zero
+// gradient), all H reads in flight before the writes.
+template <int LPR, int CPL>
+__global__ __launch_bounds__(kBlock) void touch_rows_kernel(
+    TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
+    int32_t B, float inv_b, const int32_t* __restrict__ flags, uint32_t token) {
+  if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
+  constexpr int R = kWave / LPR;
+  constexpr int H = 8;
+  const int E = d.dim, E4 = E / 4;
+  const int lane = lane_id();
+  const int rg = lane / LPR, rl = lane % LPR;
+  const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
+  const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
+  if (chunk >= nchunks) return;
+  const int lo = chunk * C, hi = min(lo + C, NS);
+  uint32_t prev = lo > 0 ? key_of(sorted[lo - 1]) : kNoKey;
+  for (int s = lo; s < hi; s += H) {
+    bool head[H];
+    int tb[H];
+    uint32_t row[H];
+#pragma unroll
+    for (int u = 0; u < H; ++u) {
+      const bool valid = s + u < hi;
+      const uint64_t p = valid ? sorted[s + u] : 0ull;
+      const uint32_t key = key_of(p);
+      head[u] = valid && key != prev;
+      prev = valid ? key : prev;
+      tb[u] = head[u] ? table_of_bag(bag_of(p), B, inv_b) : 0;
+      row[u] = head[u] ? key - d.rowbase[tb[u]] : 0u;
+    }
+    f4 v[H][CPL];
+#pragma unroll
+    for (int u = 0; u < H; ++u) {
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int c4 = rl + j * LPR;
+        if (head[u] && c4 < E4)
+          v[u][j] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(
+              static_cast<const float*>(d.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < H; ++u) {
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int c4 = rl + j * LPR;
+        if (head[u] && c4 < E4)
+          __builtin_nontemporal_store(v[u][j], reinterpret_cast<f4*>(
+              static_cast<float*>(d.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
+      }
+    }
+  }
+}
+
 int grid_bags(int64_t TB, RowGeom g) {
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   return int((TB + per_block - 1) / per_block);
@@ -227,6 +288,23 @@ hipError_t launch_owner_update(const TableDesc& d, const float* dW, const int32_
     default: EMB_OWN(4); break;
   }
 #undef EMB_OWN
+  return hipGetLastError();
+}
+
+hipError_t launch_touch_rows(const TableDesc& d, int32_t B, const BwdLayout& L, char* ws,
+                             uint32_t token, hipStream_t st) {
+  if (L.ns == 0) return hipSuccess;
+  const uint64_t* sorted = sorted_buffer(L, ws);
+  const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
+  const float inv_b = 1.0f / float(B);
+  const RowGeom g = row_geom(d.dim);
+  const int per_block = kWavesPerBlock * (kWave / g.lpr);
+  const dim3 grid(unsigned((L.nchunks + per_block - 1) / per_block));
+#define EMB_TOUCH(LL, CC)                                                                    \
+  hipLaunchKernelGGL((touch_rows_kernel<LL, CC>), grid, dim3(kBlock), 0, st, d, sorted,      \
+                     int32_t(L.ns), int32_t(L.chunk), int32_t(L.nchunks), B, inv_b, flags, token)
+  EMB_GEOM_SWITCH(g, EMB_TOUCH)
+#undef EMB_TOUCH
   return hipGetLastError();
 }
 

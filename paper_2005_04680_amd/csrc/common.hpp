@@ -158,6 +158,11 @@ hipError_t launch_owner_update(const TableDesc& d, const float* dW, const int32_
                                const int32_t* O, int64_t NS, int32_t B, int32_t owners, float lr,
                                hipStream_t st);
 
+// Floor of the update: reads and writes back (unchanged) every row that the
+// sorted look-ups of a prepared workspace touch, once.
+hipError_t launch_touch_rows(const TableDesc& d, int32_t B, const BwdLayout& L, char* ws,
+                             uint32_t token, hipStream_t st);
+
 hipError_t launch_split(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t st);
 hipError_t launch_combine(const uint16_t* hi, const uint16_t* lo, float* w, int64_t n,
                           hipStream_t st);

@@ -1,6 +1,7 @@
 """The paper's unfused update designs on the GPU (measured baselines):
 Algorithm 2 (materialised dW), Algorithm 3 with FP32 atomics, the fused
-atomic update, and Algorithm 4's row-range ownership."""
+atomic update, and Algorithm 4's row-range ownership; and the update's floor
+(each touched row read and written back once)."""
 import numpy as np
 import pytest
 import torch
@@ -72,3 +73,35 @@ def test_atomic_update_within_tolerance(fused):
     assert oracle.backward_sgd(G, B, I, O, 0.1, Wref) == 0
     for t, (a, b) in enumerate(zip(gt.host(), Wref)):
         assert_close(a, b, f"atomic table {t}")
+
+
+@pytest.mark.parametrize("dim", [16, 64, 256, 1024])
+def test_touch_rows_keeps_every_bit(dim):
+    """The floor kernel writes back what it read: the tables keep their bits,
+    and the prepared workspace still drives an update that matches the oracle."""
+    W, I, O, G, B, E = _case(11 + dim, dim=dim, hot=0.3)
+    rows = [w.shape[0] for w in W]
+    gt = GpuTables(W)
+    Id, Od = to_dev(I), to_dev(O)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(len(W), B, I.size, E), dtype=torch.uint8,
+                     device=DEV)
+    assert pk.embbag_backward_prepare(rows, E, B, Id, Od, ws, gt.status) == 0
+    for _ in range(2):
+        assert pk.embbag_baseline_touch_rows(B, I.size, gt.w, ws) == 0
+    for a, b in zip(gt.host(), W):
+        assert bits_equal(a, b)
+    assert pk.embbag_backward_apply_sgd(to_dev(G), B, I.size, 0.1, gt.w, ws) == 0
+    assert gt.read_status() == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd(G, B, I, O, 0.1, Wref) == 0
+    for t, (a, b) in enumerate(zip(gt.host(), Wref)):
+        assert_close(a, b, f"table {t} after touch + apply")
+
+
+def test_touch_rows_argument_errors():
+    W, I, O, G, B, E = _case(4)
+    gt = GpuTables(W)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(len(W), B, I.size, E), dtype=torch.uint8,
+                     device=DEV)
+    assert pk.embbag_baseline_touch_rows(B, I.size, gt.w, ws[:256]) == pk.EMBBAG_ERR_WORKSPACE
+    assert pk.embbag_baseline_touch_rows(-1, I.size, gt.w, ws) == pk.EMBBAG_ERR_INVALID_ARG
