@@ -51,6 +51,11 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return before + inc - v;
 }
 
+// Scan of the per-tile digit counts: four digits (one 16-byte word of a
+// tile's row) per block, kScanPer consecutive tiles per thread and round.
+constexpr int kScanPer = 16;
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
 // Digits handled per thread when a block walks all the digits of a radix.
 template <int BITS>
 struct Radix {
@@ -129,7 +134,7 @@ __global__ __launch_bounds__(kBlock) void build_keys(
       if (s < s_hi) atomicAdd(&lhist[key & (R - 1)], 1u);
     }
     __syncthreads();
-    for (int i = tid; i < R; i += kBlock) hist[size_t(i) * ntiles + blk] = lhist[i];
+    for (int i = tid; i < R; i += kBlock) hist[size_t(blk) * R + i] = lhist[i];
   }
   if (err != 0) atomicMin(&lerr, err);
   __syncthreads();
@@ -153,12 +158,16 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restri
     if (s < NS) atomicAdd(&lhist[(key_of(src[s]) >> shift) & (R - 1)], 1u);
   }
   __syncthreads();
-  for (int i = tid; i < R; i += kBlock) hist[size_t(i) * ntiles + blk] = lhist[i];
+  for (int i = tid; i < R; i += kBlock) hist[size_t(blk) * R + i] = lhist[i];
 }
 
-// Block d < radix: exclusive scan of digit d's tile counts (in tile order) and
-// the digit total.  Block `radix` (first pass only): folds the per-block
-// status words into this call's verdict and lowers the caller's status word.
+// Block g < radix / 4 (after the XCD remap): for digits [4g, 4g + 4), the
+// exclusive scan of the
+// tile counts in tile order (hist is [tile][radix], rewritten in place: one
+// 16-byte word per tile) and the digit totals.  Thread tid takes kScanPer
+// consecutive tiles of each round of kBlock * kScanPer tiles.  The last
+// block (first pass only) folds the per-block status words into this call's
+// verdict and lowers the caller's status word.
 __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist, int32_t ntiles,
                                                      int32_t radix,
                                                      uint32_t* __restrict__ totals,
@@ -166,10 +175,10 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
                                                      int32_t nparts, int32_t* __restrict__ flags,
                                                      int32_t* __restrict__ d_status,
                                                      uint32_t token) {
-  __shared__ uint32_t scratch[kWavesPerBlock + 1];
+  __shared__ u4 wsum[kWavesPerBlock];
   __shared__ int32_t lerr;
   const int tid = threadIdx.x;
-  if (int(blockIdx.x) == radix) {
+  if (int(blockIdx.x) == radix / 4) {
     if (tid == 0) lerr = 0;
     __syncthreads();
     int e = 0;
@@ -183,17 +192,52 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
     }
     return;
   }
-  uint32_t* row = hist + size_t(blockIdx.x) * ntiles;
-  uint32_t running = 0;
-  for (int base = 0; base < ntiles; base += kBlock) {
-    const int i = base + tid;
-    const uint32_t v = i < ntiles ? row[i] : 0u;
-    uint32_t tot;
-    const uint32_t ex = block_exclusive_scan(v, scratch, &tot);
-    if (i < ntiles) row[i] = running + ex;
-    running += tot;
+  const int lane = lane_id(), w = tid / kWave;
+  // Each XCD takes one contiguous range of the digit groups, so that the
+  // blocks sharing a cache line of a tile's row share that XCD's L2.
+  const uint32_t g = xcd_remap(blockIdx.x, uint32_t(radix / 4));
+  u4* col = reinterpret_cast<u4*>(hist) + g;  // tile t's word: col[t * radix / 4]
+  const size_t stride = size_t(radix / 4);
+  u4 running = u4{0u, 0u, 0u, 0u};
+  for (int base = 0; base < ntiles; base += kBlock * kScanPer) {
+    const int t0 = base + tid * kScanPer;
+    u4 v[kScanPer];
+    u4 sum = u4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < kScanPer; ++q) {
+      v[q] = t0 + q < ntiles ? col[size_t(t0 + q) * stride] : u4{0u, 0u, 0u, 0u};
+      sum += v[q];
+    }
+    // exclusive scan of `sum` over the block, four counts at once
+    u4 inc = sum;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      u4 n;
+      n.x = __shfl_up(inc.x, off, kWave);
+      n.y = __shfl_up(inc.y, off, kWave);
+      n.z = __shfl_up(inc.z, off, kWave);
+      n.w = __shfl_up(inc.w, off, kWave);
+      if (lane >= off) inc += n;
+    }
+    if (lane == kWave - 1) wsum[w] = inc;
+    __syncthreads();
+    u4 before = u4{0u, 0u, 0u, 0u}, all = u4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+      const u4 x = wsum[i];
+      if (i < w) before += x;
+      all += x;
+    }
+    __syncthreads();  // wsum is rewritten by the next round
+    u4 ex = running + before + inc - sum;
+#pragma unroll
+    for (int q = 0; q < kScanPer; ++q) {
+      if (t0 + q < ntiles) col[size_t(t0 + q) * stride] = ex;
+      ex += v[q];
+    }
+    running += all;
   }
-  if (tid == 0) totals[blockIdx.x] = running;
+  if (tid == 0) reinterpret_cast<u4*>(totals)[g] = running;
 }
 
 // Stable scatter of one tile by the digit at `shift` (with VALS, the value
@@ -210,14 +254,32 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   __shared__ float vbuf[VALS ? TILE : 1];
   __shared__ uint32_t whist[kWavesPerBlock][R];
   __shared__ uint32_t lstart[R];
-  __shared__ uint32_t gbase[R];
+  __shared__ uint32_t gofs[R];
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
-  const int tid = threadIdx.x, blk = blockIdx.x;
+  const int tid = threadIdx.x;
+  // Each XCD takes one contiguous range of tiles: the runs that neighbouring
+  // tiles write for one digit meet in cache lines of the same L2.
+  const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
   const int lane = lane_id();
   const int w = tid / kWave;
 
+  // Wave w owns keys [w*64*IPT, (w+1)*64*IPT) of the tile, item i of lane l
+  // being key w*64*IPT + i*64 + l: ranking item by item keeps the original
+  // order.  The tile is requested first; the digit bases are computed while
+  // it is in flight.
+  const int wbase = blk * TILE + w * (kWave * IPT);
+  uint64_t item[IPT];
+  float val[VALS ? IPT : 1];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int pos = wbase + i * kWave + lane;
+    item[i] = pos < NS ? src[pos] : ~0ull;
+    if constexpr (VALS) val[i] = pos < NS ? vsrc[pos] : 0.f;
+  }
+
   // Global start of each digit's run for this tile (thread tid owns digits
-  // [tid*DPT, tid*DPT + DPT)).
+  // [tid*DPT, tid*DPT + DPT)), kept as gbase - lstart once lstart is known.
+  uint32_t gb[DPT];
   {
     uint32_t v[DPT], sum = 0;
 #pragma unroll
@@ -231,26 +293,15 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int dg = tid * DPT + i;
-      if (dg < R) gbase[dg] = ex + hist[size_t(dg) * ntiles + blk];
+      gb[i] = dg < R ? ex + hist[size_t(blk) * R + dg] : 0u;
       ex += v[i];
     }
   }
   for (int i = tid; i < kWavesPerBlock * R; i += kBlock) (&whist[0][0])[i] = 0;
   __syncthreads();
 
-  // Wave w owns keys [w*64*IPT, (w+1)*64*IPT) of the tile, item i of lane l
-  // being key w*64*IPT + i*64 + l: ranking item by item keeps the original order.
-  const int wbase = blk * TILE + w * (kWave * IPT);
-  uint64_t item[IPT];
-  float val[VALS ? IPT : 1];
   uint32_t dig[IPT];
   uint32_t rank[IPT];
-#pragma unroll
-  for (int i = 0; i < IPT; ++i) {
-    const int pos = wbase + i * kWave + lane;
-    item[i] = pos < NS ? src[pos] : ~0ull;
-    if constexpr (VALS) val[i] = pos < NS ? vsrc[pos] : 0.f;
-  }
   const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
@@ -295,7 +346,10 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int dg = tid * DPT + i;
-      if (dg < R) lstart[dg] = ex;
+      if (dg < R) {
+        lstart[dg] = ex;
+        gofs[dg] = gb[i] - ex;  // modulo 2^32: gofs + local position = global position
+      }
       ex += run[i];
     }
   }
@@ -309,13 +363,18 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
     }
   }
   __syncthreads();
+  // The locally sorted tile, written out in order: each digit's keys land in
+  // consecutive addresses.
   const int nvalid = min(TILE, NS - blk * TILE);
-  for (int j = tid; j < nvalid; j += kBlock) {
-    const uint64_t it = buf[j];
-    const uint32_t dg = (key_of(it) >> shift) & (R - 1);
-    const uint32_t to = gbase[dg] + (j - lstart[dg]);
-    dst[to] = it;
-    if constexpr (VALS) vdst[to] = vbuf[j];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int j = i * kBlock + tid;
+    if (j < nvalid) {
+      const uint64_t it = buf[j];
+      const uint32_t to = gofs[(key_of(it) >> shift) & (R - 1)] + uint32_t(j);
+      dst[to] = it;
+      if constexpr (VALS) vdst[to] = vbuf[j];
+    }
   }
 }
 
@@ -417,8 +476,8 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   // Status verdict (block R of the first scan, or alone when nothing is sorted).
   const int passes = NS > 0 ? L.passes : 0;
   if (passes == 0) {
-    hipLaunchKernelGGL(radix_scan, dim3(R + 1), dim3(kBlock), 0, st, hist, 0, R, totals, parts,
-                       nkb, flags, d_status, token);
+    hipLaunchKernelGGL(radix_scan, dim3(R / 4 + 1), dim3(kBlock), 0, st, hist, 0, R,
+                       totals, parts, nkb, flags, d_status, token);
     return hipGetLastError();
   }
   uint64_t* src = a;
@@ -430,8 +489,8 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
     if (p > 0)
       hipLaunchKernelGGL((radix_upsweep<BITS, IPT>), dim3(ntiles), dim3(kBlock), 0, st, src,
                          int32_t(NS), shift, ntiles, hist);
-    hipLaunchKernelGGL(radix_scan, dim3(p == 0 ? R + 1 : R), dim3(kBlock), 0, st, hist, ntiles, R,
-                       totals, parts, nkb, flags, d_status, token);
+    hipLaunchKernelGGL(radix_scan, dim3(R / 4 + (p == 0 ? 1 : 0)), dim3(kBlock), 0, st,
+                       hist, ntiles, R, totals, parts, nkb, flags, d_status, token);
     if (A != nullptr)
       hipLaunchKernelGGL((radix_downsweep<BITS, IPT, true>), dim3(ntiles), dim3(kBlock), 0, st,
                          src, dst, int32_t(NS), shift, ntiles, hist, totals, vsrc, vdst);
