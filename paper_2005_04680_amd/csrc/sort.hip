@@ -151,11 +151,23 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restri
   const int tid = threadIdx.x, blk = blockIdx.x;
   for (int i = tid; i < R; i += kBlock) lhist[i] = 0;
   __syncthreads();
+  // The keys arrive in the previous pass's order, so equal digits often
+  // come in runs (every copy of a hot row is adjacent): within a wavefront,
+  // the first lane of each run of equal digits adds the run's length.
   const int base = blk * (kBlock * IPT);
+  const int lane = lane_id();
 #pragma unroll 4
   for (int i = 0; i < IPT; ++i) {
     const int s = base + i * kBlock + tid;
-    if (s < NS) atomicAdd(&lhist[(key_of(src[s]) >> shift) & (R - 1)], 1u);
+    const uint32_t dg = s < NS ? (key_of(src[s]) >> shift) & (R - 1) : uint32_t(R);
+    const uint32_t left = __shfl_up(dg, 1, kWave);
+    const bool head = lane == 0 || dg != left;
+    const uint64_t heads = __builtin_amdgcn_ballot_w64(head);
+    if (head && dg < uint32_t(R)) {
+      const uint64_t after = lane == kWave - 1 ? 0ull : heads >> (lane + 1);
+      const uint32_t len = after ? uint32_t(__builtin_ctzll(after)) + 1u : uint32_t(kWave - lane);
+      atomicAdd(&lhist[dg], len);
+    }
   }
   __syncthreads();
   for (int i = tid; i < R; i += kBlock) hist[size_t(blk) * R + i] = lhist[i];
@@ -309,11 +321,17 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
     const uint32_t dg = (key_of(item[i]) >> shift) & (R - 1);
     dig[i] = dg;
     uint64_t peers = __builtin_amdgcn_ballot_w64(valid);
+    // One digit across the wavefront (a run of equal keys, common after the
+    // first pass): every valid lane is a peer.  Otherwise match bit by bit.
+    const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg);
+    if (__builtin_amdgcn_ballot_w64(valid && dg != d0) != 0) {
 #pragma unroll
-    for (int b = 0; b < BITS; ++b) {
-      const bool bit = (dg >> b) & 1u;
-      const uint64_t m = __builtin_amdgcn_ballot_w64(bit);
-      peers &= bit ? m : ~m;
+      for (int b = 0; b < BITS; ++b) {
+        // keep the lanes whose bit b equals this lane's: ~(m ^ all-ones-if-set)
+        const int32_t sb = __builtin_amdgcn_sbfe(int32_t(dg), b, 1);  // 0 or -1
+        const uint64_t m = __builtin_amdgcn_ballot_w64(sb != 0);
+        peers &= ~(m ^ uint64_t(int64_t(sb)));
+      }
     }
     const uint32_t lrank = uint32_t(__popcll(peers & below));
     const uint32_t cnt = uint32_t(__popcll(peers));
