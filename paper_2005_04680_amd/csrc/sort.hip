@@ -254,8 +254,10 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
 
 // Stable scatter of one tile by the digit at `shift` (with VALS, the value
 // of each key moves with it: vsrc[i] goes where src[i] goes).
+// Four tiles per compute unit fit when the digits have at most 9 bits and no
+// values travel along (LDS below 40 KB): registers are then held to 128.
 template <int BITS, int IPT, bool VALS>
-__global__ __launch_bounds__(kBlock) void radix_downsweep(
+__global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_downsweep(
     const uint64_t* __restrict__ src, uint64_t* __restrict__ dst, int32_t NS, int shift,
     int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals,
     const float* __restrict__ vsrc, float* __restrict__ vdst) {
@@ -264,8 +266,9 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   constexpr int TILE = kBlock * IPT;
   __shared__ uint64_t buf[TILE];
   __shared__ float vbuf[VALS ? TILE : 1];
-  __shared__ uint32_t whist[kWavesPerBlock][R];
-  __shared__ uint32_t lstart[R];
+  // per-wave digit counts, then each wave's first position for a digit in
+  // the locally sorted tile (at most TILE: 16 bits)
+  __shared__ uint16_t whist[kWavesPerBlock][R];
   __shared__ uint32_t gofs[R];
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   const int tid = threadIdx.x;
@@ -290,7 +293,8 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
   }
 
   // Global start of each digit's run for this tile (thread tid owns digits
-  // [tid*DPT, tid*DPT + DPT)), kept as gbase - lstart once lstart is known.
+  // [tid*DPT, tid*DPT + DPT)), kept as gbase - (start of the digit's run in
+  // the locally sorted tile) once that start is known.
   uint32_t gb[DPT];
   {
     uint32_t v[DPT], sum = 0;
@@ -337,7 +341,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
     const uint32_t cnt = uint32_t(__popcll(peers));
     const uint32_t prior = whist[w][dg];
     rank[i] = prior + lrank;
-    if (valid && lrank == 0) whist[w][dg] = prior + cnt;
+    if (valid && lrank == 0) whist[w][dg] = uint16_t(prior + cnt);
   }
   __syncthreads();
   {
@@ -352,7 +356,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
 #pragma unroll
         for (int ww = 0; ww < kWavesPerBlock; ++ww) {
           const uint32_t c = whist[ww][dg];
-          whist[ww][dg] = r;
+          whist[ww][dg] = uint16_t(r);
           r += c;
         }
       }
@@ -365,7 +369,8 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
     for (int i = 0; i < DPT; ++i) {
       const int dg = tid * DPT + i;
       if (dg < R) {
-        lstart[dg] = ex;
+#pragma unroll
+        for (int ww = 0; ww < kWavesPerBlock; ++ww) whist[ww][dg] = uint16_t(whist[ww][dg] + ex);
         gofs[dg] = gb[i] - ex;  // modulo 2^32: gofs + local position = global position
       }
       ex += run[i];
@@ -375,7 +380,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep(
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
     if (wbase + i * kWave + lane < NS) {
-      const uint32_t at = lstart[dig[i]] + whist[w][dig[i]] + rank[i];
+      const uint32_t at = whist[w][dig[i]] + rank[i];
       buf[at] = item[i];
       if constexpr (VALS) vbuf[at] = val[i];
     }
