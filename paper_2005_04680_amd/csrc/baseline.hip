@@ -167,6 +167,12 @@ template <int LPR, int CPL>
 __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     int32_t B, float inv_b, const int32_t* __restrict__ flags, uint32_t token) {
+  __shared__ TableLds tl;
+  if constexpr (LPR < kWave) {
+    stage_tables(d, tl);
+    __syncthreads();
+  }
+  const auto& tbl = table_view<(LPR < kWave)>(d, tl);
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
   constexpr int H = 8;
@@ -190,7 +196,7 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
       head[u] = valid && key != prev;
       prev = valid ? key : prev;
       tb[u] = head[u] ? table_of_bag(bag_of(p), B, inv_b) : 0;
-      row[u] = head[u] ? key - d.rowbase[tb[u]] : 0u;
+      row[u] = head[u] ? key - tbl.rowbase[tb[u]] : 0u;
     }
     f4 v[H][CPL];
 #pragma unroll
@@ -200,7 +206,7 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
         const int c4 = rl + j * LPR;
         if (head[u] && c4 < E4)
           v[u][j] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(
-              static_cast<const float*>(d.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
+              static_cast<const float*>(tbl.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
       }
     }
 #pragma unroll
@@ -210,7 +216,7 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
         const int c4 = rl + j * LPR;
         if (head[u] && c4 < E4)
           __builtin_nontemporal_store(v[u][j], reinterpret_cast<f4*>(
-              static_cast<float*>(d.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
+              static_cast<float*>(tbl.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
       }
     }
   }

@@ -40,6 +40,35 @@ struct TableDesc {
   int32_t dim;
 };
 
+// The per-table pointers and key bases, copied to LDS by kernels whose
+// wavefronts hold several row groups: there the table number differs per
+// lane, and a per-lane index into the kernel arguments is a vector load.
+struct TableLds {
+  void* w[kMaxTables];
+  void* lo[kMaxTables];
+  uint32_t rowbase[kMaxTables + 1];
+};
+
+// Every thread of the block must call it; a barrier must follow.
+__device__ __forceinline__ void stage_tables(const TableDesc& d, TableLds& s) {
+  const int i = threadIdx.x;
+  if (i < d.num_tables) {
+    s.w[i] = d.w[i];
+    s.lo[i] = d.lo[i];
+  }
+  if (i <= d.num_tables) s.rowbase[i] = d.rowbase[i];
+}
+
+// The LDS copy where the table number is per lane, the kernel arguments
+// (scalar loads) where it is uniform over the wavefront.
+template <bool kLds>
+__device__ __forceinline__ const auto& table_view(const TableDesc& d, const TableLds& s) {
+  if constexpr (kLds)
+    return s;
+  else
+    return d;
+}
+
 // Lane geometry for a row of E floats: LPR lanes per row (power of two), each
 // lane owning CPL groups of 4 consecutive columns, 64/LPR rows per wavefront.
 struct RowGeom {

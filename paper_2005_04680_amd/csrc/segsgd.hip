@@ -31,11 +31,13 @@ struct Fp32Rows {
   struct Pre {
     f4 w;
   };
-  static __device__ __forceinline__ Pre load(const TableDesc& d, int t, uint32_t r, int E, int c4) {
+  template <class D>
+  static __device__ __forceinline__ Pre load(const D& d, int t, uint32_t r, int E, int c4) {
     return {__builtin_nontemporal_load(
         reinterpret_cast<const f4*>(static_cast<const float*>(d.w[t]) + size_t(r) * E + c4 * 4))};
   }
-  static __device__ __forceinline__ void store(const TableDesc& d, int t, uint32_t r, int E, int c4,
+  template <class D>
+  static __device__ __forceinline__ void store(const D& d, int t, uint32_t r, int E, int c4,
                                                const Pre& p, const d4& g, double lr) {
     f4 o;
     o.x = float(double(p.w.x) - lr * g.x);
@@ -53,7 +55,8 @@ struct SplitRows {
   struct Pre {
     u2 hi, lo;
   };
-  static __device__ __forceinline__ Pre load(const TableDesc& d, int t, uint32_t r, int E, int c4) {
+  template <class D>
+  static __device__ __forceinline__ Pre load(const D& d, int t, uint32_t r, int E, int c4) {
     const size_t off = size_t(r) * E + c4 * 4;
     return {__builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.w[t]) + off)),
             __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.lo[t]) + off))};
@@ -62,7 +65,8 @@ struct SplitRows {
     const float w = __uint_as_float((hi16 << 16) | lo16);
     return float(double(w) - lr * g);
   }
-  static __device__ __forceinline__ void store(const TableDesc& d, int t, uint32_t r, int E, int c4,
+  template <class D>
+  static __device__ __forceinline__ void store(const D& d, int t, uint32_t r, int E, int c4,
                                                const Pre& p, const d4& g, double lr) {
     const uint32_t w0 = __float_as_uint(upd(p.hi.x & 0xFFFFu, p.lo.x & 0xFFFFu, g.x, lr));
     const uint32_t w1 = __float_as_uint(upd(p.hi.x >> 16, p.lo.x >> 16, g.y, lr));
@@ -136,6 +140,12 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     const void* __restrict__ dY, int32_t B, float inv_b, float lr,
     double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
+  __shared__ TableLds tl;
+  if constexpr (LPR < kWave) {
+    stage_tables(d, tl);
+    __syncthreads();
+  }
+  const auto& tb = table_view<(LPR < kWave)>(d, tl);
   // A data error, or no sort result for these sizes: no table writes.
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
@@ -168,15 +178,15 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     acc[j] = d4{0.0, 0.0, 0.0, 0.0};
     glast[j] = f4{0.f, 0.f, 0.f, 0.f};
     const int c4 = rl + j * LPR;
-    if (!first_open && c4 < E4) pre[j] = Rows::load(d, ct, cur - d.rowbase[ct], E, c4);
+    if (!first_open && c4 < E4) pre[j] = Rows::load(tb, ct, cur - tb.rowbase[ct], E, c4);
   }
 
   auto apply = [&](uint32_t key, int t) {
-    const uint32_t r = key - d.rowbase[t];
+    const uint32_t r = key - tb.rowbase[t];
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
       const int c4 = rl + j * LPR;
-      if (c4 < E4) Rows::store(d, t, r, E, c4, pre[j], acc[j], lrd);
+      if (c4 < E4) Rows::store(tb, t, r, E, c4, pre[j], acc[j], lrd);
     }
   };
 
@@ -236,11 +246,11 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
       }
       if (nseg[u]) {
         const int tu = table_of_bag(bg[u], B, inv_b);
-        const uint32_t ru = key_of(p[u]) - d.rowbase[tu];
+        const uint32_t ru = key_of(p[u]) - tb.rowbase[tu];
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
           const int c4 = rl + j * LPR;
-          if (c4 < E4) wp[u][j] = Rows::load(d, tu, ru, E, c4);
+          if (c4 < E4) wp[u][j] = Rows::load(tb, tu, ru, E, c4);
         }
       }
     }
@@ -343,6 +353,12 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
     int32_t B, float inv_b, float lr, const double* __restrict__ carry,
     const double* __restrict__ gsum, const int32_t* __restrict__ gflag,
     const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
+  __shared__ TableLds tl;
+  if constexpr (LPR < kWave) {
+    stage_tables(d, tl);
+    __syncthreads();
+  }
+  const auto& tb = table_view<(LPR < kWave)>(d, tl);
   if (flags[0] != 0 || uint32_t(flags[1]) != token) return;
   constexpr int R = kWave / LPR;
   constexpr int UF = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
@@ -358,7 +374,7 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   const uint32_t kf = key_of(sorted[lo]);
   if (kf == kl && lo > 0 && key_of(sorted[lo - 1]) == kl) return;  // began earlier
   const int ct = table_of_bag(bag_of(sorted[hi - 1]), B, inv_b);
-  const uint32_t r = kl - d.rowbase[ct];
+  const uint32_t r = kl - tb.rowbase[ct];
   const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
 
   d4 acc[CPL];
@@ -368,7 +384,7 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
     const int c4 = rl + j * LPR;
     if (c4 < E4) {
       acc[j] = *reinterpret_cast<const d4*>(carry + own * E + c4 * 4);
-      pre[j] = Rows::load(d, ct, r, E, c4);
+      pre[j] = Rows::load(tb, ct, r, E, c4);
     } else {
       acc[j] = d4{0.0, 0.0, 0.0, 0.0};
     }
@@ -419,7 +435,7 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
 #pragma unroll
   for (int j = 0; j < CPL; ++j) {
     const int c4 = rl + j * LPR;
-    if (c4 < E4) Rows::store(d, ct, r, E, c4, pre[j], acc[j], double(lr));
+    if (c4 < E4) Rows::store(tb, ct, r, E, c4, pre[j], acc[j], double(lr));
   }
 }
 

@@ -78,11 +78,19 @@ __global__ __launch_bounds__(kBlock) void build_keys(
   __shared__ uint32_t lhist[R];
   __shared__ int32_t lerr;
   __shared__ int32_t krange[2];
+  // the tables' row counts and key bases, read per look-up (a per-lane index
+  // into the kernel arguments would be a vector load for every look-up)
+  __shared__ uint32_t srows[kMaxTables];
+  __shared__ uint32_t srowbase[kMaxTables];
   const int tid = threadIdx.x;
   const int blk = blockIdx.x;
   int err = 0;
   if (tid == 0) lerr = 0;
   for (int i = tid; i < R; i += kBlock) lhist[i] = 0;
+  if (tid < d.num_tables) {
+    srows[tid] = d.rows[tid];
+    srowbase[tid] = d.rowbase[tid];
+  }
   __syncthreads();
 
   // Offsets: O[0] == 0, O non-decreasing, O[TB] == NS, all within [0, NS].
@@ -123,11 +131,11 @@ __global__ __launch_bounds__(kBlock) void build_keys(
         const uint32_t k = min(lbag[s - s_lo], uint32_t(TB - 1));
         const int t = table_of_bag(k, B, inv_b);
         int32_t r = I[s];
-        if (uint32_t(r) >= d.rows[t]) {
+        if (uint32_t(r) >= srows[t]) {
           err = min(err, EMBBAG_ERR_INDEX_RANGE);
           r = 0;
         }
-        key = d.rowbase[t] + uint32_t(r);
+        key = srowbase[t] + uint32_t(r);
         out[s] = (uint64_t(key) << 32) | k;
         if (A != nullptr) vals[s] = A[s];
       }
