@@ -95,7 +95,13 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
   int k = k0;
   int bound = s1;
   int bstart = s0;  // first look-up of bag k
+  // Several bags per row group: when their offsets O[k0..k1] fit one per
+  // lane, they are loaded together here and each bag end is then read from
+  // its lane instead of with a load of its own.
+  const bool olanes = MULTI && G < LPR;
+  int ov = 0;
   if constexpr (MULTI) {
+    if (olanes && !bad && rl <= k1 - k0) ov = O[k0 + rl];
     bound = bad ? 0 : O[k0 + 1];
     bad = bad || bound < s0 || bound > s1;
   }
@@ -179,7 +185,7 @@ __global__ __launch_bounds__(kBlock) void fwd_gather_sum(
 #pragma unroll
           for (int j = 0; j < CPL; ++j) acc[j] = d4{0.0, 0.0, 0.0, 0.0};
           ++k;
-          const int nb = O[k + 1];
+          const int nb = olanes ? __shfl(ov, rg * LPR + (k + 1 - k0), kWave) : O[k + 1];
           if (nb < bound || nb > s1) {
             bad = true;
             break;
