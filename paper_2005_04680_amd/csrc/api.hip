@@ -169,10 +169,11 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   L.nkeyblocks = L.ntiles > 0 ? L.ntiles : 1;
   // Chunk of the segmented reduce: at least 128 look-ups per wavefront (a
   // wavefront walks one chunk per row group), growing to at most 1024 while
-  // at least ~16K wavefronts remain.
+  // at least ~32K wavefronts remain (Large: 256 look-ups, 51K wavefronts;
+  // measured 2% faster than 512).
   const int64_t rgw = kWave / row_geom(E).lpr;
   int64_t c = 128 / rgw > 8 ? 128 / rgw : 8;
-  while (c < 1024 && c * 2 * 16384 * rgw <= NS) c *= 2;
+  while (c < 1024 && c * 2 * 32768 * rgw <= NS) c *= 2;
   L.chunk = c;
   L.nchunks = (NS + c - 1) / c;
   size_t off = 0;

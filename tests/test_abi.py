@@ -129,7 +129,8 @@ def test_workspace_checks(L):
 
 def test_large_workspace_is_modest():
     """Large-shaped step: 16 tables x 8192 bags x 100 look-ups, E = 256: under
-    half a GB (two 64-bit key buffers, two weight buffers, FP64 carries)."""
+    0.6 GiB (two 64-bit key buffers, two weight buffers, digit counts, FP64
+    carries) beside 98 GB of tables."""
     import paper_2005_04680_amd as pk
     n = pk.embbag_backward_workspace_bytes(16, 8192, 16 * 8192 * 100, 256)
-    assert n < 512 * 2 ** 20
+    assert n < 614 * 2 ** 20
