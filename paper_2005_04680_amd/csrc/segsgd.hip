@@ -390,22 +390,45 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
     }
   }
   // Chunks chunk+1, chunk+2, ... belong to the segment while the chunk before
-  // continues it.  At a group boundary a filled group is taken whole (the
-  // segment then continues past it); otherwise up to UF chunks, not crossing
-  // the next group boundary (their first-segment partials and the key just
-  // past them), are loaded per step.
+  // continues it.  At a group boundary the filled groups that follow are taken
+  // whole (the segment then continues past each): the flags of up to UF
+  // groups, then the sums of the leading filled ones, are requested together
+  // and added in order.  Otherwise up to UF chunks, not crossing the next
+  // group boundary (their first-segment partials and the key just past them),
+  // are loaded per step.
+  const int ngroups = (nchunks + kCarryGroup - 1) / kCarryGroup;
   bool inside = true;
   int c2 = chunk + 1;
   while (inside) {
     const int gi = c2 / kCarryGroup, off = c2 % kCarryGroup;
-    if (off == 0 && c2 < nchunks && gflag[gi] != 0) {
+    if (off == 0 && c2 < nchunks) {
+      int nf = 0;  // filled groups in a row from gi (at most UF)
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) {
-        const int c4 = rl + j * LPR;
-        if (c4 < E4) acc[j] += *reinterpret_cast<const d4*>(gsum + int64_t(gi) * E + c4 * 4);
+      for (int u = 0; u < UF; ++u) {
+        const int f = gi + u < ngroups ? gflag[gi + u] : 0;
+        nf += (nf == u && f != 0) ? 1 : 0;
       }
-      c2 += kCarryGroup;
-      continue;
+      if (nf > 0) {
+        d4 gs[UF][CPL];
+#pragma unroll
+        for (int u = 0; u < UF; ++u) {
+#pragma unroll
+          for (int j = 0; j < CPL; ++j) {
+            const int c4 = rl + j * LPR;
+            gs[u][j] = (u < nf && c4 < E4)
+                           ? *reinterpret_cast<const d4*>(gsum + int64_t(gi + u) * E + c4 * 4)
+                           : d4{0.0, 0.0, 0.0, 0.0};
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UF; ++u) {
+          if (u >= nf) break;
+#pragma unroll
+          for (int j = 0; j < CPL; ++j) acc[j] += gs[u][j];
+        }
+        c2 += nf * kCarryGroup;
+        continue;
+      }
     }
     const int n = kCarryGroup - off < UF ? kCarryGroup - off : UF;
     d4 part[UF][CPL];
