@@ -263,9 +263,10 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
 // Stable scatter of one tile by the digit at `shift` (with VALS, the value
 // of each key moves with it: vsrc[i] goes where src[i] goes).
 // Four tiles per compute unit fit when the digits have at most 9 bits and no
-// values travel along (LDS below 40 KB): registers are then held to 128.
+// values travel along (LDS below 40 KB), three with values (below 53 KB):
+// registers are then held to 128 or 168.
 template <int BITS, int IPT, bool VALS>
-__global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_downsweep(
+__global__ __launch_bounds__(kBlock, BITS <= 9 ? (VALS ? 3 : 4) : 1) void radix_downsweep(
     const uint64_t* __restrict__ src, uint64_t* __restrict__ dst, int32_t NS, int shift,
     int32_t ntiles, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals,
     const float* __restrict__ vsrc, float* __restrict__ vdst) {
@@ -274,10 +275,15 @@ __global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_do
   constexpr int TILE = kBlock * IPT;
   __shared__ uint64_t buf[TILE];
   __shared__ float vbuf[VALS ? TILE : 1];
-  // per-wave digit counts, then each wave's first position for a digit in
-  // the locally sorted tile (at most TILE: 16 bits)
-  __shared__ uint16_t whist[kWavesPerBlock][R];
-  __shared__ uint32_t gofs[R];
+  // Per-wave digit counts, then each wave's first position for a digit in
+  // the locally sorted tile (at most TILE: 16 bits); once the tile is
+  // sorted in LDS, the same memory holds each digit's global offset.
+  union WaveDigits {
+    uint16_t whist[kWavesPerBlock][R];
+    uint32_t gofs[R];
+  };
+  __shared__ WaveDigits wd;
+  auto& whist = wd.whist;
   __shared__ uint32_t scratch[kWavesPerBlock + 1];
   const int tid = threadIdx.x;
   // Each XCD takes one contiguous range of tiles: the runs that neighbouring
@@ -352,6 +358,7 @@ __global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_do
     if (valid && lrank == 0) whist[w][dg] = uint16_t(prior + cnt);
   }
   __syncthreads();
+  uint32_t go[DPT];  // global offset of each owned digit's run, minus its local start
   {
     // Per digit: offsets of each wave's run inside the tile's digit run, and
     // the start of each digit's run in the locally sorted tile.
@@ -379,8 +386,8 @@ __global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_do
       if (dg < R) {
 #pragma unroll
         for (int ww = 0; ww < kWavesPerBlock; ++ww) whist[ww][dg] = uint16_t(whist[ww][dg] + ex);
-        gofs[dg] = gb[i] - ex;  // modulo 2^32: gofs + local position = global position
       }
+      go[i] = gb[i] - ex;  // modulo 2^32: go + local position = global position
       ex += run[i];
     }
   }
@@ -394,6 +401,12 @@ __global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_do
     }
   }
   __syncthreads();
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) {
+    const int dg = tid * DPT + i;
+    if (dg < R) wd.gofs[dg] = go[i];
+  }
+  __syncthreads();
   // The locally sorted tile, written out in order: each digit's keys land in
   // consecutive addresses.
   const int nvalid = min(TILE, NS - blk * TILE);
@@ -402,7 +415,7 @@ __global__ __launch_bounds__(kBlock, (BITS <= 9 && !VALS) ? 4 : 1) void radix_do
     const int j = i * kBlock + tid;
     if (j < nvalid) {
       const uint64_t it = buf[j];
-      const uint32_t to = gofs[(key_of(it) >> shift) & (R - 1)] + uint32_t(j);
+      const uint32_t to = wd.gofs[(key_of(it) >> shift) & (R - 1)] + uint32_t(j);
       dst[to] = it;
       if constexpr (VALS) vdst[to] = vbuf[j];
     }
