@@ -22,7 +22,9 @@
  *   separate tensors).
  * Bags.  `batch` = B bags per table.  Bag k = t*B + b reads
  *   indices[offsets[k] .. offsets[k+1]) (half-open), rows of table t.
- *   `indices`: device int32 [num_indices], table-local rows.
+ *   `indices`: device int32 [num_indices], table-local rows; num_indices <=
+ *   2^31 - 1 - 2^16 (look-ups are indexed in 32 bits, with headroom for the
+ *   last radix tile and reduce chunk).
  *   `offsets`: device int32 [T*B + 1], offsets[0] == 0, non-decreasing,
  *   offsets[T*B] == num_indices.  (Algorithm 1's header swaps the two sizes;
  *   its loops read O[n] and O[n+1].)  A row may repeat within and across

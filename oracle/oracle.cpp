@@ -43,12 +43,16 @@ constexpr int kErrIndexRange = -3;
 constexpr int kErrOffsets = -4;
 
 constexpr int64_t kInt32Max = 2147483647;
+// The largest look-up count the library accepts: 2^31 - 1 - 2^16 (it indexes
+// look-ups in 32 bits with headroom), rejected alike here so that both sides
+// return the same status on the same arguments.
+constexpr int64_t kMaxIndices = kInt32Max - 65536;
 
 // Argument checks, first in the fixed validation order.
 int check_args(int32_t T, int32_t B, int32_t E, const int64_t* rows, int64_t NS) {
   if (T < 1 || T > 64) return kErrInvalidArg;
   if (E < 4 || E > 1024 || E % 4 != 0) return kErrInvalidArg;
-  if (B < 0 || NS < 0 || NS > kInt32Max) return kErrInvalidArg;
+  if (B < 0 || NS < 0 || NS > kMaxIndices) return kErrInvalidArg;
   if (rows == nullptr) return kErrInvalidArg;
   if (int64_t(T) * int64_t(B) + 1 > kInt32Max) return kErrInvalidArg;
   int64_t total = 0;

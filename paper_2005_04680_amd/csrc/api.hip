@@ -9,6 +9,10 @@ using namespace embbag;
 namespace {
 
 constexpr int64_t kInt32Max = 2147483647;
+// Look-ups per call: the kernels index look-ups in 32 bits and step up to a
+// radix tile (4096) or a reduce chunk past the last one, so 2^16 of headroom
+// below 2^31 keeps every such sum in range.
+constexpr int64_t kMaxIndices = kInt32Max - 65536;
 constexpr size_t kWsAlign = 256;
 
 bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
@@ -45,7 +49,7 @@ int make_desc(int32_t T, int32_t E, const int64_t* rows, void* const* w, void* c
 }
 
 int check_bags(int32_t T, int32_t B, const int32_t* I, const int32_t* O, int64_t NS) {
-  if (B < 0 || NS < 0 || NS > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+  if (B < 0 || NS < 0 || NS > kMaxIndices) return EMBBAG_ERR_INVALID_ARG;
   if (int64_t(T) * B + 1 > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
   if (O == nullptr || (NS > 0 && I == nullptr)) return EMBBAG_ERR_INVALID_ARG;
   // offsets[0] must be both 0 and num_indices: the sizes alone contradict.
@@ -93,7 +97,7 @@ int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_
 int apply_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16, int32_t B,
                  int64_t NS, float lr, void* ws, size_t ws_bytes, const PoolArgs& pool,
                  hipStream_t st) {
-  if (B < 0 || NS < 0 || NS > kInt32Max || int64_t(d.num_tables) * B + 1 > kInt32Max)
+  if (B < 0 || NS < 0 || NS > kMaxIndices || int64_t(d.num_tables) * B + 1 > kInt32Max)
     return EMBBAG_ERR_INVALID_ARG;
   if (int64_t(d.num_tables) * B == 0 && NS > 0) return EMBBAG_ERR_OFFSETS;
   if (NS > 0 && (dY == nullptr || !aligned(dY, dy_bf16 ? 8 : 16))) return EMBBAG_ERR_INVALID_ARG;
@@ -263,7 +267,7 @@ size_t embbag_backward_workspace_bytes(int32_t num_tables, int32_t batch, int64_
                                        int32_t dim) {
   if (num_tables < 1 || num_tables > kMaxTables || dim < 4 || dim > 1024 || dim % 4 != 0)
     return 0;
-  if (batch < 0 || num_indices < 0 || num_indices > kInt32Max) return 0;
+  if (batch < 0 || num_indices < 0 || num_indices > kMaxIndices) return 0;
   if (int64_t(num_tables) * batch + 1 > kInt32Max) return 0;
   return backward_layout(num_tables, batch, num_indices, dim, 0, false).total;
 }
@@ -440,7 +444,7 @@ int embbag_combine_fp32(const uint16_t* hi, const uint16_t* lo, float* w, int64_
 
 size_t embbag_dedup_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices) {
   if (num_tables < 1 || num_tables > kMaxTables) return 0;
-  if (batch < 0 || num_indices < 0 || num_indices > kInt32Max) return 0;
+  if (batch < 0 || num_indices < 0 || num_indices > kMaxIndices) return 0;
   if (int64_t(num_tables) * batch + 1 > kInt32Max) return 0;
   return backward_layout(num_tables, batch, num_indices, 4, 0, true).total;
 }
@@ -477,7 +481,7 @@ int embbag_baseline_materialize(const float* grad_pooled, int32_t num_tables, in
     return EMBBAG_ERR_INVALID_ARG;
   int rc = check_bags(num_tables, batch, nullptr, offsets, 0);
   if (rc) return rc;
-  if (num_indices < 0 || num_indices > kInt32Max) return EMBBAG_ERR_INVALID_ARG;
+  if (num_indices < 0 || num_indices > kMaxIndices) return EMBBAG_ERR_INVALID_ARG;
   if (int64_t(num_tables) * batch > 0 && (grad_pooled == nullptr || !aligned(grad_pooled, 16)))
     return EMBBAG_ERR_INVALID_ARG;
   if (num_indices > 0 && (dW == nullptr || !aligned(dW, 16))) return EMBBAG_ERR_INVALID_ARG;
@@ -541,7 +545,7 @@ int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_
   int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
                      reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
   if (rc) return rc;
-  if (batch < 0 || num_indices < 0 || num_indices > kInt32Max ||
+  if (batch < 0 || num_indices < 0 || num_indices > kMaxIndices ||
       int64_t(d.num_tables) * batch + 1 > kInt32Max)
     return EMBBAG_ERR_INVALID_ARG;
   if (int64_t(d.num_tables) * batch == 0 && num_indices > 0) return EMBBAG_ERR_OFFSETS;

@@ -80,6 +80,7 @@ def _tables(rows, dim, ptrs=None):
     ((10,), 8, -1, 1, -1),           # B < 0
     ((10,), 8, 1, -1, -1),           # NS < 0
     ((10,), 8, 1, 2 ** 31, -1),      # NS > INT32_MAX
+    ((10,), 8, 1, 2 ** 31 - 2 ** 16, -1),  # NS above the 2^31 - 1 - 2^16 limit
     ((10,), 8, 0, 5, -4),            # T*B == 0 but NS > 0
 ])
 def test_forward_argument_errors(L, rows, dim, batch, ns, expect):

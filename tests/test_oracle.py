@@ -302,6 +302,9 @@ def test_status_codes(oracle):
     assert oracle.validate(rows, 8, -1, I, O) == oracle.ERR_INVALID_ARG
     assert oracle.validate(rows, 8, 2, I, O, num_tables=0) == oracle.ERR_INVALID_ARG
     assert oracle.validate((10, 0), 8, 2, I, O) == oracle.ERR_INVALID_ARG
+    # more look-ups than the library accepts (2^31 - 1 - 2^16): rejected with the
+    # arguments, before the arrays are read
+    assert oracle.validate(rows, 8, 2, I, O, num_indices=2 ** 31 - 2 ** 16) == oracle.ERR_INVALID_ARG
     bad = O.copy(); bad[0] = 1
     assert oracle.validate(rows, 8, 2, I, bad) == oracle.ERR_OFFSETS
     bad = np.array([0, 2, 1, 3, 4], np.int32)
