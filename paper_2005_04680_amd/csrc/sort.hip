@@ -343,13 +343,18 @@ __global__ __launch_bounds__(kBlock, BITS <= 9 ? (VALS ? 3 : 4) : 1) void radix_
     // first pass): every valid lane is a peer.  Otherwise match bit by bit.
     const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg);
     if (__builtin_amdgcn_ballot_w64(valid && dg != d0) != 0) {
+      uint32_t plo = uint32_t(peers), phi = uint32_t(peers >> 32);
 #pragma unroll
       for (int b = 0; b < BITS; ++b) {
-        // keep the lanes whose bit b equals this lane's: ~(m ^ all-ones-if-set)
+        // keep the lanes whose bit b equals this lane's: peers & ~(m ^ s), s
+        // all ones where the bit is set; one three-input logic op per half
+        // (truth table 0x90 = f(0xF0, 0xCC, 0xAA) for f(a, b, c) = a & ~(b ^ c))
         const int32_t sb = __builtin_amdgcn_sbfe(int32_t(dg), b, 1);  // 0 or -1
         const uint64_t m = __builtin_amdgcn_ballot_w64(sb != 0);
-        peers &= ~(m ^ uint64_t(int64_t(sb)));
+        plo = __builtin_amdgcn_bitop3_b32(plo, uint32_t(m), uint32_t(sb), 0x90);
+        phi = __builtin_amdgcn_bitop3_b32(phi, uint32_t(m >> 32), uint32_t(sb), 0x90);
       }
+      peers = (uint64_t(phi) << 32) | plo;
     }
     const uint32_t lrank = uint32_t(__popcll(peers & below));
     const uint32_t cnt = uint32_t(__popcll(peers));
