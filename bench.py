@@ -311,9 +311,10 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(the tables shard table-wise across GPUs by design, "
-                                   "but no multi-GPU path is built)"}))
+        print(json.dumps({"error": "the library runs on one GPU; --gpus must be 1 "
+                                   "(the tables would shard table-wise across GPUs, with an "
+                                   "all-to-all of pooled rows and gradients, but no multi-GPU "
+                                   "path is implemented)"}))
         sys.exit(2)
 
     import torch
