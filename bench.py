@@ -428,10 +428,33 @@ def main():
         rc = prep(bt)
         return rc if rc else apply(bt)
 
-    for i in range(args.warmup):
-        bt = batches[i % len(batches)]
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream(device=dev) if args.overlap_prepare else main
+
+    def step(bt, prev, evs=None):
+        """One step: prepare (on `side`, after `prev`), forward, apply; returns
+        the event after the apply.  `evs` (six timing events) bracket the calls."""
+        e_f0, e_f1, e_p0, e_p1, e_a0, e_a1 = evs if evs is not None else tuple(
+            torch.cuda.Event(enable_timing=False) for _ in range(6))
+        side.wait_event(prev)
+        with torch.cuda.stream(side):
+            e_p0.record(side)
+            pk.check(prep(bt), "prepare")
+            e_p1.record(side)
+        e_f0.record(main)
         pk.check(fwd(bt), "forward")
-        pk.check(bwd(bt), "backward")
+        e_f1.record(main)
+        main.wait_event(e_p1)
+        e_a0.record(main)
+        pk.check(apply(bt), "apply")
+        e_a1.record(main)
+        return e_a1
+
+    # warm-up in the same stream pattern as the timed steps
+    prev = torch.cuda.Event()
+    prev.record(main)
+    for i in range(args.warmup):
+        prev = step(batches[i % len(batches)], prev)
     torch.cuda.synchronize()
     pk.check(pk.embbag_status_read(status), "device status")
 
@@ -441,8 +464,6 @@ def main():
     # gathers rows; the apply phase waits for both, and the next step's
     # prepare waits for this step's apply, which still reads the workspace.
     K = args.steps
-    main = torch.cuda.current_stream()
-    side = torch.cuda.Stream(device=dev) if args.overlap_prepare else main
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(6)) for _ in range(K)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -450,21 +471,7 @@ def main():
     start.record(main)
     prev_apply = start
     for i in range(K):
-        bt = batches[i % len(batches)]
-        e_f0, e_f1, e_p0, e_p1, e_a0, e_a1 = ev[i]
-        side.wait_event(prev_apply)
-        with torch.cuda.stream(side):
-            e_p0.record(side)
-            prep(bt)
-            e_p1.record(side)
-        e_f0.record(main)
-        fwd(bt)
-        e_f1.record(main)
-        main.wait_event(e_p1)
-        e_a0.record(main)
-        apply(bt)
-        e_a1.record(main)
-        prev_apply = e_a1
+        prev_apply = step(batches[i % len(batches)], prev_apply, ev[i])
     stop.record(main)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
