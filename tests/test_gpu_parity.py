@@ -232,7 +232,8 @@ def test_split_bf16_activation_argument_errors():
 # Integer work: bit-exact
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("case", ["tiny", "random", "p1_hot", "small", "mlperf_scaled",
-                                  "tile1024", "tile2048", "tile4096"])
+                                  "tile1024", "tile2048", "tile4096", "one_pass", "digits7",
+                                  "four_passes"])
 def test_dedup_bit_exact(case):
     rng = np.random.default_rng(5)
     if case == "tiny":
@@ -253,6 +254,14 @@ def test_dedup_bit_exact(case):
         cfg = scaled(get_config("mlperf"), batch=8192)
         rows, batch = cfg.rows, cfg.batch
         I, O = make_batch(cfg, 0)
+    elif case in ("one_pass", "digits7", "four_passes"):
+        # key widths the other cases miss (the dedup needs row counts only, no
+        # tables): 9-bit keys sorted in one pass, 21-bit keys in three passes of
+        # 7 bits, and 31-bit keys (1.6G rows in all) in four passes of 8 bits
+        rows, batch, pool = {"one_pass": ((300, 200), 3000, 40),
+                             "digits7": ((1500000, 500000), 20000, 50),
+                             "four_passes": ((2 ** 30, 1000, 2 ** 29), 5000, 60)}[case]
+        I, O = random_bags(rng, rows, batch, pool, 0.05, 0.3)
     else:
         # radix tiles of 1024, 2048 and 4096 keys: 12-bit keys (6-bit digits)
         # over 300K look-ups; 17-bit keys (9-bit digits) over 400K and 3M
