@@ -43,7 +43,7 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
 }
 
 template <int LPR, int CPL, bool SPLIT, bool MULTI, int MODE, bool YBF16>
-__global__ __launch_bounds__(kBlock) void fwd_gather_sum(
+__global__ __launch_bounds__(kBlock, MULTI ? 6 : 1) void fwd_gather_sum(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, int32_t G, int32_t groups_per_table, int32_t items, void* __restrict__ Y,
     int32_t* __restrict__ status, const float* __restrict__ A) {
