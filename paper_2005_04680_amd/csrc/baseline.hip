@@ -162,11 +162,12 @@ __global__ __launch_bounds__(kWave) void owner_update_kernel(TableDesc d,
 // workspace are cut into the same chunks as the fused update's; a row group
 // walks its chunk H look-ups at a time, and for each segment that begins
 // there reads the row and writes it back unchanged (an SGD step with a zero
-// gradient), all H reads in flight before the writes.
+// gradient), all H reads in flight before the writes.  The chunks are walked
+// in the fused update's order for FP32 gradients.
 template <int LPR, int CPL>
 __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
-    int32_t B, float inv_b, const int32_t* __restrict__ flags, uint32_t token) {
+    int32_t B, float inv_b, const int32_t* __restrict__ flags, uint32_t token, int32_t in_order) {
   __shared__ TableLds tl;
   if constexpr (LPR < kWave) {
     stage_tables(d, tl);
@@ -179,7 +180,7 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
   const int E = d.dim, E4 = E / 4;
   const int lane = lane_id();
   const int rg = lane / LPR, rl = lane % LPR;
-  const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
+  const int blk = int(logical_block(in_order != 0));
   const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
   const int lo = chunk * C, hi = min(lo + C, NS);
@@ -306,9 +307,11 @@ hipError_t launch_touch_rows(const TableDesc& d, int32_t B, const BwdLayout& L, 
   const RowGeom g = row_geom(d.dim);
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const dim3 grid(unsigned((L.nchunks + per_block - 1) / per_block));
+  const int32_t in_order = apply_in_dispatch_order(grid.x, d.num_tables, B, d.dim, 4);
 #define EMB_TOUCH(LL, CC)                                                                    \
   hipLaunchKernelGGL((touch_rows_kernel<LL, CC>), grid, dim3(kBlock), 0, st, d, sorted,      \
-                     int32_t(L.ns), int32_t(L.chunk), int32_t(L.nchunks), B, inv_b, flags, token)
+                     int32_t(L.ns), int32_t(L.chunk), int32_t(L.nchunks), B, inv_b, flags, token, \
+                     in_order)
   EMB_GEOM_SWITCH(g, EMB_TOUCH)
 #undef EMB_TOUCH
   return hipGetLastError();

@@ -13,6 +13,9 @@ constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kBlock = 256;        // threads per workgroup (4 waves)
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kNumXcd = 8;         // MI355X: 8 XCDs, each with its own L2
+constexpr int kNumCu = 256;        // compute units (32 per XCD)
+constexpr int kMaxBlocksPerCu = 8; // 32 wavefronts per CU, 4 per block
+constexpr int64_t kMallBytes = int64_t(256) << 20;  // Infinity Cache (MALL)
 
 // Radix sort geometry: digits of 6..10 bits, tiles of 256 threads x 4, 8 or
 // 16 keys.
@@ -91,6 +94,35 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t n) {
   const uint32_t xcd = b % kNumXcd, idx = b / kNumXcd;
   const uint32_t q = n / kNumXcd, r = n % kNumXcd;
   return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+// Order in which a grid walks its logical blocks (bags or chunks in table
+// order).  With per-XCD ranges (xcd_remap) each XCD works through its own
+// tables: the rows a table reuses stay in that XCD's L2, but about
+// kNumXcd + resident / blocks_per_table tables are in flight at once, one or
+// more per XCD.  In dispatch order the resident blocks form one window over
+// the grid, about 1 + resident / blocks_per_table tables wide, that every XCD
+// shares: each L2 then sees more tables, but the MALL, which serves the
+// reuse the L2s miss, holds fewer.  Dispatch order is taken when the grid does
+// not fit the chip at once and the reused data of the tables that per-XCD
+// ranges put in flight (per_table_bytes each) exceeds half of the MALL (the
+// rest of it carries the streams that pass through).
+inline bool dispatch_order(int64_t blocks, int32_t num_tables, int64_t per_table_bytes) {
+  const int64_t resident = int64_t(kNumCu) * kMaxBlocksPerCu;
+  if (blocks <= resident || num_tables <= 0) return false;
+  const double in_flight = double(kNumXcd) + double(resident) * num_tables / double(blocks);
+  return in_flight * double(per_table_bytes) > double(kMallBytes) / 2;
+}
+
+// The update's order: a table's reused data there is its dY, B rows of E
+// gradients of dy_bytes each.
+inline bool apply_in_dispatch_order(int64_t blocks, int32_t T, int32_t B, int32_t E,
+                                    int dy_bytes) {
+  return dispatch_order(blocks, T, int64_t(B) * E * dy_bytes);
+}
+
+__device__ __forceinline__ uint32_t logical_block(bool in_dispatch_order) {
+  return in_dispatch_order ? blockIdx.x : xcd_remap(blockIdx.x, gridDim.x);
 }
 
 __device__ __forceinline__ int wave_id() {

@@ -5,9 +5,12 @@
 // flight per lane before any of them is summed, and a bag's FP32 sum is
 // stored when the walk crosses the bag's end offset (empty bags store +0.0).
 // Every lane holds CPL groups of 4 columns, so a row is read with 128-bit
-// loads (64-bit for the BF16 halves of a split table).  Blocks are remapped
-// so that each XCD walks one contiguous range of bags: those bags belong to
-// one or two tables, whose hot rows then stay in that XCD's L2.
+// loads (64-bit for the BF16 halves of a split table).  Grids that fit the
+// chip at once give each XCD one contiguous range of bags (one or two tables,
+// whose hot rows then stay in that XCD's L2).  Larger grids whose tables'
+// touched rows would not fit the MALL eight tables at a time walk the bags
+// in dispatch order: all XCDs share the table in progress, and a row read
+// again is served by the MALL instead of HBM.
 #include "common.hpp"
 
 namespace embbag {
@@ -46,14 +49,14 @@ template <int LPR, int CPL, bool SPLIT, bool MULTI, int MODE, bool YBF16>
 __global__ __launch_bounds__(kBlock, MULTI ? 6 : 1) void fwd_gather_sum(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, int32_t G, int32_t groups_per_table, int32_t items, void* __restrict__ Y,
-    int32_t* __restrict__ status, const float* __restrict__ A) {
+    int32_t* __restrict__ status, const float* __restrict__ A, int32_t in_order) {
   constexpr int R = kWave / LPR;
   constexpr int U = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
   const int E = d.dim;
   const int E4 = E / 4;
   const int lane = lane_id();
   const int rg = lane / LPR, rl = lane % LPR;
-  const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
+  const int blk = int(logical_block(in_order != 0));
   const int item = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (item >= items) return;
 
@@ -229,21 +232,22 @@ __global__ void fwd_empty_check(const int32_t* __restrict__ O, int32_t NS,
 template <bool SPLIT, int MODE, bool YBF16, int LPR, int CPL>
 void launch_one(dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I, const int32_t* O,
                 int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items, void* Y,
-                int32_t* status, const float* A) {
+                int32_t* status, const float* A, int32_t in_order) {
   if (G > 1)
     hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, true, MODE, YBF16>), grid, dim3(kBlock), 0,
-                       st, d, I, O, NS, B, G, gpt, items, Y, status, A);
+                       st, d, I, O, NS, B, G, gpt, items, Y, status, A, in_order);
   else
     hipLaunchKernelGGL((fwd_gather_sum<LPR, CPL, SPLIT, false, MODE, YBF16>), grid, dim3(kBlock),
-                       0, st, d, I, O, NS, B, G, gpt, items, Y, status, A);
+                       0, st, d, I, O, NS, B, G, gpt, items, Y, status, A, in_order);
 }
 
 template <bool SPLIT, int MODE, bool YBF16 = false>
 bool dispatch(RowGeom g, dim3 grid, hipStream_t st, const TableDesc& d, const int32_t* I,
               const int32_t* O, int32_t NS, int32_t B, int32_t G, int32_t gpt, int32_t items,
-              void* Y, int32_t* status, const float* A) {
-#define EMB_FWD(L, C) \
-  launch_one<SPLIT, MODE, YBF16, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status, A)
+              void* Y, int32_t* status, const float* A, int32_t in_order) {
+#define EMB_FWD(L, C)                                                                   \
+  launch_one<SPLIT, MODE, YBF16, L, C>(grid, st, d, I, O, NS, B, G, gpt, items, Y, status, A, \
+                                       in_order)
   switch (g.lpr) {
     case 1: EMB_FWD(1, 1); return true;
     case 2: EMB_FWD(2, 1); return true;
@@ -285,19 +289,25 @@ hipError_t launch_forward(const TableDesc& d, bool split, int32_t B, const int32
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const dim3 grid(unsigned((items + per_block - 1) / per_block));
   const int32_t ns = int32_t(NS), it = int32_t(items);
+  // A table's touched rows are at most its look-ups' rows.
+  const int64_t row_bytes = int64_t(d.dim) * (split ? 2 : 4);
+  const int32_t in_order = dispatch_order(grid.x, d.num_tables, NS / d.num_tables * row_bytes);
   bool ok = false;
   if (split && y_bf16)
     ok = dispatch<true, kPoolPlain, true>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status,
-                                          nullptr);
+                                          nullptr, in_order);
   else if (split)
-    ok = dispatch<true, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
+    ok = dispatch<true, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr,
+                                    in_order);
   else if (pool.mode == kPoolWeighted)
     ok = dispatch<false, kPoolWeighted>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status,
-                                        pool.weights);
+                                        pool.weights, in_order);
   else if (pool.mode == kPoolMean)
-    ok = dispatch<false, kPoolMean>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
+    ok = dispatch<false, kPoolMean>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr,
+                                    in_order);
   else
-    ok = dispatch<false, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr);
+    ok = dispatch<false, kPoolPlain>(g, grid, st, d, I, O, ns, B, G, gpt, it, Y, status, nullptr,
+                                     in_order);
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();
 }

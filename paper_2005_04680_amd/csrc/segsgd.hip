@@ -17,8 +17,11 @@
 // that does not depend on scheduling (the result is bit-reproducible).
 //
 // Locality: each XCD owns one contiguous range of chunks, so the dY rows it
-// gathers at any time belong to one or two tables; the W rows, touched once,
-// are read and written with non-temporal hints so they do not evict them.
+// gathers at any time belong to one or two tables, unless eight tables' dY
+// would fill more than half of the MALL: then the chunks are walked in
+// dispatch order, and all XCDs gather from the dY of the table in progress,
+// which the MALL holds.  The W rows, touched once, are read and written with
+// non-temporal hints so they do not evict dY.
 #include <type_traits>
 
 #include "common.hpp"
@@ -139,7 +142,8 @@ template <int LPR, int CPL, class Rows, int MODE, bool GBF16>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     const void* __restrict__ dY, int32_t B, float inv_b, float lr,
-    double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token, PoolDev pd) {
+    double* __restrict__ carry, const int32_t* __restrict__ flags, uint32_t token, PoolDev pd,
+    int32_t in_order) {
   __shared__ TableLds tl;
   if constexpr (LPR < kWave) {
     stage_tables(d, tl);
@@ -156,7 +160,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   const int E4 = E / 4;  // float4 groups per row
   const int lane = lane_id();
   const int rg = lane / LPR, rl = lane % LPR;
-  const int blk = int(xcd_remap(blockIdx.x, gridDim.x));
+  const int blk = int(logical_block(in_order != 0));
   const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
   const int lo = chunk * C, hi = min(lo + C, NS);
@@ -465,10 +469,12 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
 template <class Rows, int MODE, bool GBF16>
 bool launch_seg(RowGeom g, int blocks, hipStream_t st, const TableDesc& d, const uint64_t* sorted,
                 int32_t NS, int32_t C, int32_t nchunks, const void* dY, int32_t B, float inv_b,
-                float lr, double* carry, const int32_t* flags, uint32_t token, PoolDev pd) {
+                float lr, double* carry, const int32_t* flags, uint32_t token, PoolDev pd,
+                int32_t in_order) {
 #define EMB_SEG(L, CC)                                                                     \
   hipLaunchKernelGGL((segment_sgd<L, CC, Rows, MODE, GBF16>), dim3(blocks), dim3(kBlock), 0, st, \
-                     d, sorted, NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token, pd)
+                     d, sorted, NS, C, nchunks, dY, B, inv_b, lr, carry, flags, token, pd,      \
+                     in_order)
   switch (g.lpr) {
     case 1: EMB_SEG(1, 1); return true;
     case 2: EMB_SEG(2, 1); return true;
@@ -556,8 +562,9 @@ bool launch_apply(const TableDesc& d, int32_t B, const void* dY, float lr, const
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const int blocks = int((L.nchunks + per_block - 1) / per_block);
   const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
+  const int32_t in_order = apply_in_dispatch_order(blocks, d.num_tables, B, d.dim, GBF16 ? 2 : 4);
   return launch_seg<Rows, MODE, GBF16>(g, blocks, st, d, sorted, NS, C, nch, dY, B, inv_b, lr,
-                                       carry, flags, token, pd) &&
+                                       carry, flags, token, pd, in_order) &&
          launch_group(g, st, sorted, NS, C, nch, d.dim, int32_t(L.ngroups), carry, gsum, gflag,
                       flags, token) &&
          launch_fix<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry, gsum,
