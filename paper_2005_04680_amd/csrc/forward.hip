@@ -51,7 +51,10 @@ __global__ __launch_bounds__(kBlock, MULTI ? 6 : 1) void fwd_gather_sum(
     int32_t B, int32_t G, int32_t groups_per_table, int32_t items, void* __restrict__ Y,
     int32_t* __restrict__ status, const float* __restrict__ A, int32_t in_order) {
   constexpr int R = kWave / LPR;
-  constexpr int U = CPL == 1 ? 8 : (CPL == 2 ? 4 : 2);
+  // Row loads in flight per lane: 10 when a wavefront reads one 1 KB row per
+  // load and walks one bag (58 VGPRs, still 8 waves per SIMD); fewer as the
+  // rows per lane grow.
+  constexpr int U = CPL == 1 ? (LPR == kWave && !MULTI ? 10 : 8) : (CPL == 2 ? 4 : 2);
   const int E = d.dim;
   const int E4 = E / 4;
   const int lane = lane_id();
@@ -154,10 +157,17 @@ __global__ __launch_bounds__(kBlock, MULTI ? 6 : 1) void fwd_gather_sum(
       int idx;
       if constexpr (kWin) {
         if constexpr (LPR == kWave) {
-          idx = __builtin_amdgcn_readlane(vcur, ss - wbase);
+          // U need not divide LPR: the last slots of an iteration may lie in
+          // the next window, which is already loaded (off < LPR + U <= 2 LPR).
+          const int off = ss - wbase;
+          idx = off < LPR ? __builtin_amdgcn_readlane(vcur, off)
+                          : __builtin_amdgcn_readlane(vnext, off - LPR);
           if constexpr (MODE == kPoolWeighted)
-            wt[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(acur), ss - wbase));
+            wt[u] = __int_as_float(off < LPR
+                                       ? __builtin_amdgcn_readlane(__float_as_int(acur), off)
+                                       : __builtin_amdgcn_readlane(__float_as_int(anext), off - LPR));
         } else {
+          static_assert(LPR % U == 0, "a window must hold whole iterations");
           idx = __shfl(vcur, rg * LPR + (ss - wbase), kWave);
           if constexpr (MODE == kPoolWeighted) wt[u] = __shfl(acur, rg * LPR + (ss - wbase), kWave);
         }
