@@ -112,6 +112,20 @@ def test_many_tiles_and_long_segments(pool, batch, hot):
     check_step(W, batch, I, O, G, 0.1, what=f"tiles P<={pool}")
 
 
+def test_dispatch_block_order():
+    """Grids large enough that the forward (16384 blocks) and the update (4272
+    blocks) walk their blocks in dispatch order rather than in per-XCD ranges:
+    4 tables x 65536 bags of 0-16 look-ups (2.19M) at E = 128, where eight
+    tables' rows and dY would not fit half of the MALL.  Row 0 of each table
+    takes 30% of its look-ups, a segment across thousands of chunks."""
+    rng = np.random.default_rng(77)
+    rows, batch, dim = (200000,) * 4, 65536, 128
+    I, O = random_bags(rng, rows, batch, 16, 0.02, 0.3)
+    W = _tables(rng, rows, dim, 0.01)
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    check_step(W, batch, I, O, G, 0.1, what="dispatch order")
+
+
 @pytest.mark.parametrize("dim,seed", [(16, 1), (64, 2), (64, 3), (256, 4)])
 def test_segments_of_many_lengths(dim, seed):
     """Segments of every length from 1 to tens of thousands of look-ups, in random
