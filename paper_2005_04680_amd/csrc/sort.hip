@@ -84,6 +84,16 @@ __global__ __launch_bounds__(kBlock) void build_keys(
   __shared__ uint32_t srowbase[kMaxTables];
   const int tid = threadIdx.x;
   const int blk = blockIdx.x;
+  const int s_lo = blk * TILE;
+  const int s_hi = min(s_lo + TILE, NS);
+  // The tile's indices are requested first, so that they arrive while the
+  // bag search below runs.
+  int32_t rv[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int s = s_lo + i * kBlock + tid;
+    rv[i] = s < s_hi ? I[s] : 0;
+  }
   int err = 0;
   if (tid == 0) lerr = 0;
   for (int i = tid; i < R; i += kBlock) lhist[i] = 0;
@@ -101,8 +111,6 @@ __global__ __launch_bounds__(kBlock) void build_keys(
     if (k < TB && O[k + 1] < o) err = EMBBAG_ERR_OFFSETS;
   }
 
-  const int s_lo = blk * TILE;
-  const int s_hi = min(s_lo + TILE, NS);
   if (s_lo < s_hi) {  // uniform over the block
     for (int i = tid; i < TILE; i += kBlock) lbag[i] = 0;
     if (tid < 2) {
@@ -123,14 +131,14 @@ __global__ __launch_bounds__(kBlock) void build_keys(
       for (int s = a; s < b; ++s) lbag[s - s_lo] = uint32_t(k);
     }
     __syncthreads();
-#pragma unroll 4
+#pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int s = s_lo + i * kBlock + tid;
       uint32_t key = 0;
       if (s < s_hi) {
         const uint32_t k = min(lbag[s - s_lo], uint32_t(TB - 1));
         const int t = table_of_bag(k, B, inv_b);
-        int32_t r = I[s];
+        int32_t r = rv[i];
         if (uint32_t(r) >= srows[t]) {
           err = min(err, EMBBAG_ERR_INDEX_RANGE);
           r = 0;
