@@ -112,6 +112,20 @@ def test_many_tiles_and_long_segments(pool, batch, hot):
     check_step(W, batch, I, O, G, 0.1, what=f"tiles P<={pool}")
 
 
+@pytest.mark.parametrize("dim,split", [(200, False), (256, False), (256, True)])
+def test_long_bags_one_row_per_wavefront(dim, split):
+    """Bags of up to 300 look-ups at E = 200 and 256 (one row per wavefront,
+    10 row loads in flight per lane): an iteration's last slots take their
+    indices from the next 64-entry window at every offset."""
+    rng = np.random.default_rng(dim + 11 + split)
+    rows = (5000, 300)
+    batch = 97
+    W = _tables(rng, rows, dim, 0.05)
+    I, O = random_bags(rng, rows, batch, 300, empty_frac=0.05, hot_frac=0.2)
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    check_step(W, batch, I, O, G, 0.1, split=split, what=f"long bags E={dim} split={split}")
+
+
 def test_dispatch_block_order():
     """Grids large enough that the forward (16384 blocks) and the update (4272
     blocks) walk their blocks in dispatch order rather than in per-XCD ranges:
@@ -532,7 +546,7 @@ def test_apply_needs_a_prepared_workspace():
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("dim", [16, 64, 128, 256, 1024])
 @pytest.mark.parametrize("mode", ["weighted", "mean"])
-@pytest.mark.parametrize("maxp", [3, 40])
+@pytest.mark.parametrize("maxp", [3, 40, 300])
 def test_weighted_and_mean(dim, mode, maxp):
     import paper_2005_04680_amd as pk
     rng = np.random.default_rng(dim * 3 + maxp + (mode == "mean"))
