@@ -63,6 +63,9 @@ struct Radix {
   static constexpr int DPT = R > kBlock ? R / kBlock : 1;
 };
 
+// Offsets read per thread before the first is used, in build_keys.
+constexpr int kOq = 8;
+
 // Bags, keys and the first digit's histogram for one tile; offsets checks for
 // a slice of the bags; one status word per block.  With per-look-up weights
 // A, vals[s] = A[s] starts the value array that the sort carries along.
@@ -104,31 +107,68 @@ __global__ __launch_bounds__(kBlock) void build_keys(
   __syncthreads();
 
   // Offsets: O[0] == 0, O non-decreasing, O[TB] == NS, all within [0, NS].
+  // kOq offsets per thread are requested before any is checked (with one
+  // look-up per bag a block checks thousands of them).
   const int kb0 = blk * vb, kb1 = min(kb0 + vb, TB + 1);
-  for (int k = kb0 + tid; k < kb1; k += kBlock) {
-    const int o = O[k];
-    if (o < 0 || o > NS || (k == 0 && o != 0) || (k == TB && o != NS)) err = EMBBAG_ERR_OFFSETS;
-    if (k < TB && O[k + 1] < o) err = EMBBAG_ERR_OFFSETS;
+  for (int64_t k0 = kb0 + tid; k0 < kb1; k0 += kBlock * kOq) {
+    int oa[kOq], ob[kOq];
+#pragma unroll
+    for (int q = 0; q < kOq; ++q) {
+      const int64_t k = k0 + q * kBlock;
+      oa[q] = k < kb1 ? O[k] : 0;
+      ob[q] = k < kb1 && k < TB ? O[k + 1] : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < kOq; ++q) {
+      const int64_t k = k0 + q * kBlock;
+      if (k >= kb1) break;
+      const int o = oa[q];
+      if (o < 0 || o > NS || (k == 0 && o != 0) || (k == TB && o != NS)) err = EMBBAG_ERR_OFFSETS;
+      if (k < TB && ob[q] < o) err = EMBBAG_ERR_OFFSETS;
+    }
   }
 
   if (s_lo < s_hi) {  // uniform over the block
     for (int i = tid; i < TILE; i += kBlock) lbag[i] = 0;
-    if (tid < 2) {
-      // last bag k in [0, TB - 1] with O[k] <= x (binary search; O monotone
-      // when valid, and clamped so a bad O still stays in bounds)
-      const int x = tid == 0 ? s_lo : s_hi - 1;
+    const int w = tid / kWave;
+    if (w < 2) {
+      // Last bag k in [0, TB - 1] with O[k] <= x, for the tile's first
+      // (wave 0) and last (wave 1) look-up: a 64-way search, each lane
+      // probing one of 64 evenly spaced bags of the current range per round
+      // (ceil(log64 TB) dependent loads).  O[lo] <= x holds for valid O; a bad
+      // O still leaves the range inside [0, TB - 1].
+      const int lane = lane_id();
+      const int x = w == 0 ? s_lo : s_hi - 1;
       int lo = 0, hi = TB - 1;
       while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (O[mid] <= x) lo = mid; else hi = mid - 1;
+        const int step = int((int64_t(hi) - lo + kWave) / kWave);  // ceil((hi - lo + 1) / 64)
+        const int64_t k = lo + int64_t(lane) * step;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(k <= hi && O[k] <= x);
+        const int j = m != 0 ? 63 - __builtin_clzll(m) : 0;
+        lo = lo + j * step;
+        hi = int(min(int64_t(lo) + step - 1, int64_t(hi)));
       }
-      krange[tid] = lo;
+      if (lane == 0) krange[w] = lo;
     }
     __syncthreads();
-    // Expand bag ids over the tile's look-ups.
-    for (int k = krange[0] + tid; k <= krange[1]; k += kBlock) {
-      const int a = max(O[k], s_lo), b = min(O[k + 1], s_hi);
-      for (int s = a; s < b; ++s) lbag[s - s_lo] = uint32_t(k);
+    // Expand bag ids over the tile's look-ups (kOq bags per thread requested
+    // together).
+    const int k1 = krange[1];
+    for (int64_t k0 = krange[0] + tid; k0 <= k1; k0 += kBlock * kOq) {
+      int oa[kOq], ob[kOq];
+#pragma unroll
+      for (int q = 0; q < kOq; ++q) {
+        const int64_t k = k0 + q * kBlock;
+        oa[q] = k <= k1 ? O[k] : 0;
+        ob[q] = k <= k1 ? O[k + 1] : 0;
+      }
+#pragma unroll
+      for (int q = 0; q < kOq; ++q) {
+        const int64_t k = k0 + q * kBlock;
+        if (k > k1) break;
+        const int a = max(oa[q], s_lo), b = min(ob[q], s_hi);
+        for (int s = a; s < b; ++s) lbag[s - s_lo] = uint32_t(k);
+      }
     }
     __syncthreads();
 #pragma unroll
@@ -170,12 +210,19 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restri
   // The keys arrive in the previous pass's order, so equal digits often
   // come in runs (every copy of a hot row is adjacent): within a wavefront,
   // the first lane of each run of equal digits adds the run's length.
+  // All of the thread's keys are requested before the first is counted.
   const int base = blk * (kBlock * IPT);
   const int lane = lane_id();
-#pragma unroll 4
+  uint32_t kv[IPT];
+#pragma unroll
   for (int i = 0; i < IPT; ++i) {
     const int s = base + i * kBlock + tid;
-    const uint32_t dg = s < NS ? (key_of(src[s]) >> shift) & (R - 1) : uint32_t(R);
+    kv[i] = s < NS ? key_of(src[s]) : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int s = base + i * kBlock + tid;
+    const uint32_t dg = s < NS ? (kv[i] >> shift) & (R - 1) : uint32_t(R);
     const uint32_t left = __shfl_up(dg, 1, kWave);
     const bool head = lane == 0 || dg != left;
     const uint64_t heads = __builtin_amdgcn_ballot_w64(head);
@@ -319,19 +366,23 @@ __global__ __launch_bounds__(kBlock, BITS <= 9 ? (VALS ? 3 : 4) : 1) void radix_
   // the locally sorted tile) once that start is known.
   uint32_t gb[DPT];
   {
-    uint32_t v[DPT], sum = 0;
+    // the tile's own counts are requested with the totals (they do not
+    // depend on the scan)
+    uint32_t v[DPT], th[DPT], sum = 0;
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int dg = tid * DPT + i;
       v[i] = dg < R ? totals[dg] : 0u;
-      sum += v[i];
+      th[i] = dg < R ? hist[size_t(blk) * R + dg] : 0u;
     }
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) sum += v[i];
     uint32_t tot;
     uint32_t ex = block_exclusive_scan(sum, scratch, &tot);
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int dg = tid * DPT + i;
-      gb[i] = dg < R ? ex + hist[size_t(blk) * R + dg] : 0u;
+      gb[i] = dg < R ? ex + th[i] : 0u;
       ex += v[i];
     }
   }
