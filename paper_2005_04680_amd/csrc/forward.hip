@@ -45,8 +45,11 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
 }
 
+// Row groups that walk several bags are held to 6 waves per SIMD (80 VGPRs)
+// for one float4 group per lane and plain sums, 5 for weighted or mean
+// pooling (their coefficients take registers); wider rows take what they need.
 template <int LPR, int CPL, bool SPLIT, bool MULTI, int MODE, bool YBF16>
-__global__ __launch_bounds__(kBlock, MULTI ? 6 : 1) void fwd_gather_sum(
+__global__ __launch_bounds__(kBlock, MULTI ? (CPL == 1 && MODE == kPoolPlain ? 6 : (CPL == 1 ? 5 : 1)) : 1) void fwd_gather_sum(
     TableDesc d, const int32_t* __restrict__ I, const int32_t* __restrict__ O, int32_t NS,
     int32_t B, int32_t G, int32_t groups_per_table, int32_t items, void* __restrict__ Y,
     int32_t* __restrict__ status, const float* __restrict__ A, int32_t in_order) {

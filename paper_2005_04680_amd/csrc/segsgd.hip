@@ -330,15 +330,28 @@ __global__ __launch_bounds__(kBlock) void carry_group(
                     key_of(sorted[first - 1]) == key_of(sorted[after]);
   if (rl == 0) gflag[g] = full ? 1 : 0;
   if (!full) return;
+  // The partials are requested GU at a time (all 16 for one float4 group per
+  // lane, 2 for three or four) and added in chunk order.
+  constexpr int GU = CPL == 1 ? kCarryGroup : (CPL == 2 ? kCarryGroup / 2 : kCarryGroup / 8);
   d4 acc[CPL];
 #pragma unroll
   for (int j = 0; j < CPL; ++j) acc[j] = d4{0.0, 0.0, 0.0, 0.0};
-#pragma unroll 4
-  for (int u = 0; u < kCarryGroup; ++u) {
+#pragma unroll 1
+  for (int u0 = 0; u0 < kCarryGroup; u0 += GU) {
+    d4 v[GU][CPL];
 #pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-      const int c4 = rl + j * LPR;
-      if (c4 < E4) acc[j] += *reinterpret_cast<const d4*>(carry + 2 * (c0 + u) * E + c4 * 4);
+    for (int u = 0; u < GU; ++u) {
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
+        const int c4 = rl + j * LPR;
+        v[u][j] = c4 < E4 ? *reinterpret_cast<const d4*>(carry + 2 * (c0 + u0 + u) * E + c4 * 4)
+                          : d4{0.0, 0.0, 0.0, 0.0};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < GU; ++u) {
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) acc[j] += v[u][j];
     }
   }
 #pragma unroll
@@ -373,11 +386,14 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   if (chunk >= nchunks) return;
   const int lo = chunk * C, hi = min(lo + C, NS);
   if (hi >= NS) return;
-  const uint32_t kl = key_of(sorted[hi - 1]);
-  if (key_of(sorted[hi]) != kl) return;             // last segment ends here
-  const uint32_t kf = key_of(sorted[lo]);
-  if (kf == kl && lo > 0 && key_of(sorted[lo - 1]) == kl) return;  // began earlier
-  const int ct = table_of_bag(bag_of(sorted[hi - 1]), B, inv_b);
+  // the words around both ends of the chunk, requested together
+  const uint64_t wl = sorted[hi - 1], wn = sorted[hi], wf = sorted[lo];
+  const uint64_t wb = lo > 0 ? sorted[lo - 1] : ~0ull;
+  const uint32_t kl = key_of(wl);
+  if (key_of(wn) != kl) return;             // last segment ends here
+  const uint32_t kf = key_of(wf);
+  if (kf == kl && lo > 0 && key_of(wb) == kl) return;  // began earlier
+  const int ct = table_of_bag(bag_of(wl), B, inv_b);
   const uint32_t r = kl - tb.rowbase[ct];
   const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
 
@@ -395,40 +411,58 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   }
   // Chunks chunk+1, chunk+2, ... belong to the segment while the chunk before
   // continues it.  At a group boundary the filled groups that follow are taken
-  // whole (the segment then continues past each): the flags of up to UF
-  // groups, then the sums of the leading filled ones, are requested together
-  // and added in order.  Otherwise up to UF chunks, not crossing the next
-  // group boundary (their first-segment partials and the key just past them),
-  // are loaded per step.
+  // whole (the segment then continues past each): the flags of the next
+  // groups (one per lane of the row group when it has at least 16 lanes,
+  // else UF), then the sums of the leading filled ones, UF at a time, are
+  // requested and added in order.  Otherwise up to UF chunks, not crossing
+  // the next group boundary (their first-segment partials and the key just
+  // past them), are loaded per step.
+  constexpr bool kLaneFlags = LPR >= 16;
+  constexpr int NF = kLaneFlags ? LPR : UF;  // flags read per step
   const int ngroups = (nchunks + kCarryGroup - 1) / kCarryGroup;
+  int unfilled = -1;  // a group known not to be filled
   bool inside = true;
   int c2 = chunk + 1;
   while (inside) {
     const int gi = c2 / kCarryGroup, off = c2 % kCarryGroup;
-    if (off == 0 && c2 < nchunks) {
-      int nf = 0;  // filled groups in a row from gi (at most UF)
-#pragma unroll
-      for (int u = 0; u < UF; ++u) {
-        const int f = gi + u < ngroups ? gflag[gi + u] : 0;
-        nf += (nf == u && f != 0) ? 1 : 0;
-      }
-      if (nf > 0) {
-        d4 gs[UF][CPL];
+    if (off == 0 && c2 < nchunks && gi != unfilled) {
+      int nf = 0;  // filled groups in a row from gi (at most NF)
+      if constexpr (kLaneFlags) {
+        const int f = gi + rl < ngroups ? gflag[gi + rl] : 0;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(f != 0);
+        uint64_t mine;
+        if constexpr (LPR == kWave)
+          mine = m;
+        else
+          mine = (m >> (rg * LPR)) & ((1ull << LPR) - 1ull);
+        nf = ~mine == 0ull ? kWave : int(__builtin_ctzll(~mine));
+      } else {
 #pragma unroll
         for (int u = 0; u < UF; ++u) {
-#pragma unroll
-          for (int j = 0; j < CPL; ++j) {
-            const int c4 = rl + j * LPR;
-            gs[u][j] = (u < nf && c4 < E4)
-                           ? *reinterpret_cast<const d4*>(gsum + int64_t(gi + u) * E + c4 * 4)
-                           : d4{0.0, 0.0, 0.0, 0.0};
-          }
+          const int f = gi + u < ngroups ? gflag[gi + u] : 0;
+          nf += (nf == u && f != 0) ? 1 : 0;
         }
+      }
+      if (nf < NF) unfilled = gi + nf;
+      if (nf > 0) {
+        for (int u0 = 0; u0 < nf; u0 += UF) {
+          d4 gs[UF][CPL];
 #pragma unroll
-        for (int u = 0; u < UF; ++u) {
-          if (u >= nf) break;
+          for (int u = 0; u < UF; ++u) {
 #pragma unroll
-          for (int j = 0; j < CPL; ++j) acc[j] += gs[u][j];
+            for (int j = 0; j < CPL; ++j) {
+              const int c4 = rl + j * LPR;
+              gs[u][j] = (u0 + u < nf && c4 < E4)
+                             ? *reinterpret_cast<const d4*>(gsum + int64_t(gi + u0 + u) * E + c4 * 4)
+                             : d4{0.0, 0.0, 0.0, 0.0};
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < UF; ++u) {
+            if (u0 + u >= nf) break;
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) acc[j] += gs[u][j];
+          }
         }
         c2 += nf * kCarryGroup;
         continue;
