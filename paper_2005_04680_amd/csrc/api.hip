@@ -160,11 +160,12 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
   L.bits = L.passes > 0 ? (nbits + L.passes - 1) / L.passes : 6;
   if (L.bits < 6) L.bits = 6;
   // Radix tiles: the largest of 4096, 2048 or 1024 keys that still gives at
-  // least 512 tiles (two per compute unit), but at least 4 keys per digit
-  // value (a tile's scatter then writes runs, not single words).  Sizes only
-  // shrink as the key width grows, so the workspace computed without the
-  // table sizes (6-bit digits) covers every call.
-  const int ipt_min = (1 << L.bits) / 64 > 4 ? (1 << L.bits) / 64 : 4;
+  // least 512 tiles (two per compute unit), but at least 2 keys per digit
+  // value (a tile's scatter then writes runs, not single words; 1.7M keys of
+  // 10-bit digits: 832 tiles of 2048 sort faster than 416 of 4096).  Sizes
+  // only shrink as the key width grows, so the workspace computed without
+  // the table sizes (6-bit digits) covers every call.
+  const int ipt_min = (1 << L.bits) / 128 > 4 ? (1 << L.bits) / 128 : 4;
   L.ipt = kMaxItemsPerThread;
   while (L.ipt > ipt_min &&
          (NS + int64_t(kBlock) * L.ipt - 1) / (int64_t(kBlock) * L.ipt) < 512)
