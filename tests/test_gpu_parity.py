@@ -161,6 +161,26 @@ def test_segments_of_many_lengths(dim, seed):
     check_step(W, batch, look, O, G, 0.1, what=f"segment lengths E={dim}")
 
 
+@pytest.mark.parametrize("dim", [256, 512])
+def test_segment_past_one_flag_read(dim):
+    """One row takes 250K of ~345K look-ups: at E >= 256 (64 lanes per row, chunks
+    of 128 look-ups) its segment fills about 120 groups of 16 chunks, more than
+    the 64 group flags the fix-up reads at a time, so the fix-up reads the next
+    64 flags after a read that found every group filled."""
+    rng = np.random.default_rng(dim + 5)
+    M = 64
+    mult = np.concatenate([[250000], rng.integers(1, 3000, M - 1)])
+    look = np.repeat(rng.permutation(M), mult).astype(np.int32)
+    rng.shuffle(look)
+    NS = look.size
+    batch = NS // 50 + 1
+    cuts = np.sort(rng.integers(0, NS + 1, batch - 1))
+    O = np.concatenate([[0], cuts, [NS]]).astype(np.int32)
+    W = _tables(rng, (M,), dim, 0.01)
+    G = rng.standard_normal((1, batch, dim)).astype(np.float32)
+    check_step(W, batch, look, O, G, 0.1, what=f"segment past one flag read E={dim}")
+
+
 def test_small_full():
     """Small-shaped workload at full size: 8 x 1e6 x 64, B=2048, P=32, Zipf(1.05)."""
     cfg = get_config("small")
