@@ -4,7 +4,9 @@ Argument marshalling only: every function takes torch tensors that live on
 the GPU, passes their device pointers and the current HIP stream to the C ABI
 of ``libembbag.so`` (declared in ``include/embbag.h``) and returns its status
 code.  All computation happens in the library's HIP kernels; there is no CPU
-path, and loading fails loudly when the library has not been built.
+path, and loading fails loudly when the library has not been built.  The
+buffer sizes the C ABI takes on trust (table widths, offsets, activations,
+outputs) are checked here against the call's sizes first (ValueError).
 
 Operators (arXiv 2005.04680): Algorithm 1 (sum-pooled forward), Algorithms
 2-3 fused into one backward + sparse SGD update of the touched rows, and the
@@ -141,9 +143,53 @@ def _dt(*names):
     return tuple(getattr(torch, n) for n in names if hasattr(torch, n))
 
 
+# Buffer shapes the C ABI assumes but cannot check (it takes raw pointers): a
+# table narrower than `dim`, or an offsets, activation or output buffer shorter
+# than its sizes imply, would let a kernel read or write past its end.  These
+# checks raise ValueError before any library call.  Sizes the library itself
+# rejects (a negative batch, no tables) are left to its status codes.
+def _need(ok, msg):
+    if not ok:
+        raise ValueError(msg)
+
+
+def _check_bags(T, batch, offsets):
+    if offsets is not None and T >= 1 and batch >= 0:
+        _need(offsets.numel() == T * batch + 1,
+              f"offsets: {offsets.numel()} entries, expected num_tables * batch + 1 = "
+              f"{T * batch + 1}")
+
+
+def _check_numel(t, n, name, exact=True):
+    if t is not None and n >= 0:
+        ok = t.numel() == n if exact else t.numel() >= n
+        _need(ok, f"{name}: {t.numel()} elements, expected {'' if exact else 'at least '}{n}")
+
+
+def _check_act(t, T, batch, dim, name):
+    if T >= 1 and batch >= 0:
+        _check_numel(t, T * batch * dim, f"{name} (num_tables x batch x dim)")
+
+
+def _check_tables(tables, what="table"):
+    if len(tables) == 0:
+        return 0
+    dim = int(tables[0].shape[1]) if len(tables[0].shape) == 2 else -1
+    for i, t in enumerate(tables):
+        _need(len(t.shape) == 2 and int(t.shape[1]) == dim,
+              f"{what} {i}: shape {tuple(t.shape)}, expected 2-D with {dim} columns like {what} 0")
+    return dim
+
+
 def _tables_struct(tables, split_lo=None):
     import torch
     T = len(tables)
+    _check_tables(tables, "table" if split_lo is None else "hi table")
+    if split_lo is not None:
+        _need(len(split_lo) == T, f"{len(split_lo)} lo tables for {T} hi tables")
+        for i, (h, l) in enumerate(zip(tables, split_lo)):
+            _need(tuple(l.shape) == tuple(h.shape),
+                  f"lo table {i}: shape {tuple(l.shape)} differs from its hi half {tuple(h.shape)}")
     rows = (C.c_int64 * max(T, 1))(*[int(t.shape[0]) for t in tables])
     dim = int(tables[0].shape[1]) if T else 0
     ptrs = (C.c_void_p * max(T, 1))(*[_ptr(t, None, "table") for t in tables])
@@ -163,6 +209,7 @@ def _tables_struct(tables, split_lo=None):
 
 def _split_struct_fwd(hi):
     T = len(hi)
+    _check_tables(hi, "hi table")
     rows = (C.c_int64 * max(T, 1))(*[int(t.shape[0]) for t in hi])
     ptrs = (C.c_void_p * max(T, 1))(*[_ptr(t, None, "hi table") for t in hi])
     s = _SplitTables(T, int(hi[0].shape[1]) if T else 0, C.cast(rows, C.POINTER(C.c_int64)),
@@ -171,6 +218,11 @@ def _split_struct_fwd(hi):
 
 
 _I32 = ("int32",)
+
+
+def _status_ptr(d_status):
+    _check_numel(d_status, 1, "d_status", exact=False)
+    return _ptr(d_status, _dt(*_I32), "d_status")
 _U16 = ("uint16", "int16")
 _U32 = ("uint32", "int32")
 
@@ -178,40 +230,50 @@ _U32 = ("uint32", "int32")
 # ---- entry points (same names as the C ABI) --------------------------------
 def embbag_forward(weights, batch, indices, offsets, pooled_out, d_status=None, stream=None) -> int:
     """Algorithm 1 over FP32 tables ``weights`` (list of [M_t, E] tensors)."""
+    _check_bags(len(weights), batch, offsets)
+    _check_act(pooled_out, len(weights), batch, _check_tables(weights), "pooled_out")
     s, keep = _tables_struct(weights)
     return lib().embbag_forward(C.byref(s), int(batch), _ptr(indices, _dt(*_I32), "indices"),
                                 _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
                                 _ptr(pooled_out, _dt("float32"), "pooled_out"),
-                                _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+                                _status_ptr(d_status), _stream(stream))
 
 
 def embbag_forward_pooled(weights, batch, indices, offsets, pooled_out, per_sample_weights=None,
                           pooling=EMBBAG_POOL_SUM, d_status=None, stream=None) -> int:
     """Weighted-sum (one weight per look-up) or mean pooling over FP32 tables."""
+    _check_bags(len(weights), batch, offsets)
+    _check_act(pooled_out, len(weights), batch, _check_tables(weights), "pooled_out")
+    _check_numel(per_sample_weights, indices.numel(), "per_sample_weights")
     s, keep = _tables_struct(weights)
     return lib().embbag_forward_pooled(C.byref(s), int(batch), _ptr(indices, _dt(*_I32), "indices"),
                                        _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
                                        _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"),
                                        int(pooling), _ptr(pooled_out, _dt("float32"), "pooled_out"),
-                                       _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+                                       _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_sgd_pooled(grad_pooled, batch, indices, offsets, lr, weights, workspace,
                                per_sample_weights=None, pooling=EMBBAG_POOL_SUM, d_status=None,
                                stream=None) -> int:
+    _check_bags(len(weights), batch, offsets)
+    _check_act(grad_pooled, len(weights), batch, _check_tables(weights), "grad_pooled")
+    _check_numel(per_sample_weights, indices.numel(), "per_sample_weights")
     s, keep = _tables_struct(weights)
     return lib().embbag_backward_sgd_pooled(
         _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
         _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
         int(indices.numel()), _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"),
         int(pooling), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
-        int(workspace.numel() * workspace.element_size()), _ptr(d_status, _dt(*_I32), "d_status"),
+        int(workspace.numel() * workspace.element_size()), _status_ptr(d_status),
         _stream(stream))
 
 
 def embbag_backward_prepare_pooled(rows, dim, batch, indices, offsets, workspace,
                                    per_sample_weights=None, pooling=EMBBAG_POOL_SUM,
                                    d_status=None, stream=None) -> int:
+    _check_bags(len(rows), batch, offsets)
+    _check_numel(per_sample_weights, indices.numel(), "per_sample_weights")
     T = len(rows)
     r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
     return lib().embbag_backward_prepare_pooled(
@@ -219,12 +281,15 @@ def embbag_backward_prepare_pooled(rows, dim, batch, indices, offsets, workspace
         _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
         _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"), int(pooling),
         _ptr(workspace, None, "workspace"), int(workspace.numel() * workspace.element_size()),
-        _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+        _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_apply_sgd_pooled(grad_pooled, batch, offsets, num_indices, lr, weights,
                                      workspace, per_sample_weights=None,
                                      pooling=EMBBAG_POOL_SUM, stream=None) -> int:
+    _check_bags(len(weights), batch, offsets)
+    _check_act(grad_pooled, len(weights), batch, _check_tables(weights), "grad_pooled")
+    _check_numel(per_sample_weights, int(num_indices), "per_sample_weights")
     s, keep = _tables_struct(weights)
     return lib().embbag_backward_apply_sgd_pooled(
         _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
@@ -236,13 +301,15 @@ def embbag_backward_apply_sgd_pooled(grad_pooled, batch, offsets, num_indices, l
 
 def embbag_forward_split_bf16(hi, batch, indices, offsets, pooled_out, d_status=None,
                               stream=None) -> int:
+    _check_bags(len(hi), batch, offsets)
+    _check_act(pooled_out, len(hi), batch, _check_tables(hi, "hi table"), "pooled_out")
     s, keep = _split_struct_fwd(hi)
     return lib().embbag_forward_split_bf16(C.byref(s), int(batch),
                                            _ptr(indices, _dt(*_I32), "indices"),
                                            _ptr(offsets, _dt(*_I32), "offsets"),
                                            int(indices.numel()),
                                            _ptr(pooled_out, _dt("float32"), "pooled_out"),
-                                           _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+                                           _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_workspace_bytes(num_tables, batch, num_indices, dim) -> int:
@@ -253,29 +320,34 @@ def embbag_backward_workspace_bytes(num_tables, batch, num_indices, dim) -> int:
 def embbag_backward_sgd(grad_pooled, batch, indices, offsets, lr, weights, workspace,
                         d_status=None, stream=None) -> int:
     """Fused backward + SGD; ``weights`` are updated in place."""
+    _check_bags(len(weights), batch, offsets)
+    _check_act(grad_pooled, len(weights), batch, _check_tables(weights), "grad_pooled")
     s, keep = _tables_struct(weights)
     return lib().embbag_backward_sgd(_ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
                                      _ptr(indices, _dt(*_I32), "indices"),
                                      _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
                                      float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
                                      int(workspace.numel() * workspace.element_size()),
-                                     _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+                                     _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_sgd_split_bf16(grad_pooled, batch, indices, offsets, lr, hi, lo, workspace,
                                    d_status=None, stream=None) -> int:
+    _check_bags(len(hi), batch, offsets)
+    _check_act(grad_pooled, len(hi), batch, _check_tables(hi, "hi table"), "grad_pooled")
     s, keep = _tables_struct(hi, split_lo=lo)
     return lib().embbag_backward_sgd_split_bf16(
         _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
         _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
         int(indices.numel()), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
         int(workspace.numel() * workspace.element_size()),
-        _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+        _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_prepare(rows, dim, batch, indices, offsets, workspace, d_status=None,
                             stream=None) -> int:
     """Phase 1 of the backward: keys, validation and the sort, into ``workspace``."""
+    _check_bags(len(rows), batch, offsets)
     T = len(rows)
     r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
     return lib().embbag_backward_prepare(T, C.cast(r, C.c_void_p), int(dim), int(batch),
@@ -283,12 +355,13 @@ def embbag_backward_prepare(rows, dim, batch, indices, offsets, workspace, d_sta
                                          _ptr(offsets, _dt(*_I32), "offsets"),
                                          int(indices.numel()), _ptr(workspace, None, "workspace"),
                                          int(workspace.numel() * workspace.element_size()),
-                                         _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+                                         _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_apply_sgd(grad_pooled, batch, num_indices, lr, weights, workspace,
                               stream=None) -> int:
     """Phase 2 of the backward: segment sums and the SGD apply on FP32 tables."""
+    _check_act(grad_pooled, len(weights), batch, _check_tables(weights), "grad_pooled")
     s, keep = _tables_struct(weights)
     return lib().embbag_backward_apply_sgd(_ptr(grad_pooled, _dt("float32"), "grad_pooled"),
                                            int(batch), int(num_indices), float(lr), C.byref(s),
@@ -299,6 +372,7 @@ def embbag_backward_apply_sgd(grad_pooled, batch, num_indices, lr, weights, work
 
 def embbag_backward_apply_sgd_split_bf16(grad_pooled, batch, num_indices, lr, hi, lo, workspace,
                                          stream=None) -> int:
+    _check_act(grad_pooled, len(hi), batch, _check_tables(hi, "hi table"), "grad_pooled")
     s, keep = _tables_struct(hi, split_lo=lo)
     return lib().embbag_backward_apply_sgd_split_bf16(
         _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch), int(num_indices), float(lr),
@@ -313,29 +387,34 @@ _BF16 = ("bfloat16",) + _U16
 
 def embbag_forward_split_bf16_act(hi, batch, indices, offsets, pooled_out, d_status=None,
                                   stream=None) -> int:
+    _check_bags(len(hi), batch, offsets)
+    _check_act(pooled_out, len(hi), batch, _check_tables(hi, "hi table"), "pooled_out")
     s, keep = _split_struct_fwd(hi)
     return lib().embbag_forward_split_bf16_act(C.byref(s), int(batch),
                                                _ptr(indices, _dt(*_I32), "indices"),
                                                _ptr(offsets, _dt(*_I32), "offsets"),
                                                int(indices.numel()),
                                                _ptr(pooled_out, _dt(*_BF16), "pooled_out"),
-                                               _ptr(d_status, _dt(*_I32), "d_status"),
+                                               _status_ptr(d_status),
                                                _stream(stream))
 
 
 def embbag_backward_sgd_split_bf16_act(grad_pooled, batch, indices, offsets, lr, hi, lo,
                                        workspace, d_status=None, stream=None) -> int:
+    _check_bags(len(hi), batch, offsets)
+    _check_act(grad_pooled, len(hi), batch, _check_tables(hi, "hi table"), "grad_pooled")
     s, keep = _tables_struct(hi, split_lo=lo)
     return lib().embbag_backward_sgd_split_bf16_act(
         _ptr(grad_pooled, _dt(*_BF16), "grad_pooled"), int(batch),
         _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
         int(indices.numel()), float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
         int(workspace.numel() * workspace.element_size()),
-        _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+        _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_apply_sgd_split_bf16_act(grad_pooled, batch, num_indices, lr, hi, lo,
                                              workspace, stream=None) -> int:
+    _check_act(grad_pooled, len(hi), batch, _check_tables(hi, "hi table"), "grad_pooled")
     s, keep = _tables_struct(hi, split_lo=lo)
     return lib().embbag_backward_apply_sgd_split_bf16_act(
         _ptr(grad_pooled, _dt(*_BF16), "grad_pooled"), int(batch), int(num_indices), float(lr),
@@ -344,11 +423,15 @@ def embbag_backward_apply_sgd_split_bf16_act(grad_pooled, batch, num_indices, lr
 
 
 def embbag_split_fp32(w, hi, lo, stream=None) -> int:
+    _check_numel(hi, w.numel(), "hi")
+    _check_numel(lo, w.numel(), "lo")
     return lib().embbag_split_fp32(_ptr(w, _dt("float32"), "w"), _ptr(hi, _dt(*_U16), "hi"),
                                    _ptr(lo, _dt(*_U16), "lo"), int(w.numel()), _stream(stream))
 
 
 def embbag_combine_fp32(hi, lo, w, stream=None) -> int:
+    _check_numel(hi, w.numel(), "hi")
+    _check_numel(lo, w.numel(), "lo")
     return lib().embbag_combine_fp32(_ptr(hi, _dt(*_U16), "hi"), _ptr(lo, _dt(*_U16), "lo"),
                                      _ptr(w, _dt("float32"), "w"), int(w.numel()), _stream(stream))
 
@@ -359,6 +442,11 @@ def embbag_dedup_workspace_bytes(num_tables, batch, num_indices) -> int:
 
 def embbag_dedup(rows, batch, indices, offsets, sorted_keys, sorted_bags, unique_keys, seg_off,
                  d_num_unique, workspace, d_status=None, stream=None) -> int:
+    _check_bags(len(rows), batch, offsets)
+    for a, n in ((sorted_keys, "sorted_keys"), (sorted_bags, "sorted_bags"), (unique_keys, "unique_keys")):
+        _check_numel(a, indices.numel(), n, exact=False)
+    _check_numel(seg_off, indices.numel() + 1, "seg_off", exact=False)
+    _check_numel(d_num_unique, 1, "d_num_unique", exact=False)
     T = len(rows)
     r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
     return lib().embbag_dedup(T, C.cast(r, C.c_void_p), int(batch),
@@ -371,43 +459,52 @@ def embbag_dedup(rows, batch, indices, offsets, sorted_keys, sorted_bags, unique
                               _ptr(d_num_unique, _dt(*_I32), "d_num_unique"),
                               _ptr(workspace, None, "workspace"),
                               int(workspace.numel() * workspace.element_size()),
-                              _ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+                              _status_ptr(d_status), _stream(stream))
 
 
 # ---- baselines: the paper's unfused designs (for measurement) --------------
 def embbag_baseline_materialize(grad_pooled, num_tables, batch, dim, offsets, num_indices, dW,
                                 d_status=None, stream=None) -> int:
+    _check_bags(int(num_tables), batch, offsets)
+    _check_act(grad_pooled, int(num_tables), batch, int(dim), "grad_pooled")
+    _check_numel(dW, int(num_indices) * int(dim), "dW", exact=False)
     return lib().embbag_baseline_materialize(_ptr(grad_pooled, _dt("float32"), "grad_pooled"),
                                              int(num_tables), int(batch), int(dim),
                                              _ptr(offsets, _dt(*_I32), "offsets"),
                                              int(num_indices), _ptr(dW, _dt("float32"), "dW"),
-                                             _ptr(d_status, _dt(*_I32), "d_status"),
+                                             _status_ptr(d_status),
                                              _stream(stream))
 
 
 def embbag_baseline_update_atomic(dW, batch, indices, offsets, lr, weights, d_status=None,
                                   stream=None) -> int:
+    _check_bags(len(weights), batch, offsets)
+    _check_numel(dW, indices.numel() * _check_tables(weights), "dW", exact=False)
     s, keep = _tables_struct(weights)
     return lib().embbag_baseline_update_atomic(_ptr(dW, _dt("float32"), "dW"), int(batch),
                                                _ptr(indices, _dt(*_I32), "indices"),
                                                _ptr(offsets, _dt(*_I32), "offsets"),
                                                int(indices.numel()), float(lr), C.byref(s),
-                                               _ptr(d_status, _dt(*_I32), "d_status"),
+                                               _status_ptr(d_status),
                                                _stream(stream))
 
 
 def embbag_baseline_backward_sgd_atomic(grad_pooled, batch, indices, offsets, lr, weights,
                                         d_status=None, stream=None) -> int:
+    _check_bags(len(weights), batch, offsets)
+    _check_act(grad_pooled, len(weights), batch, _check_tables(weights), "grad_pooled")
     s, keep = _tables_struct(weights)
     return lib().embbag_baseline_backward_sgd_atomic(
         _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
         _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
-        int(indices.numel()), float(lr), C.byref(s), _ptr(d_status, _dt(*_I32), "d_status"),
+        int(indices.numel()), float(lr), C.byref(s), _status_ptr(d_status),
         _stream(stream))
 
 
 def embbag_baseline_update_owner(dW, batch, indices, offsets, lr, weights, owners,
                                  stream=None) -> int:
+    _check_bags(len(weights), batch, offsets)
+    _check_numel(dW, indices.numel() * _check_tables(weights), "dW", exact=False)
     s, keep = _tables_struct(weights)
     return lib().embbag_baseline_update_owner(_ptr(dW, _dt("float32"), "dW"), int(batch),
                                               _ptr(indices, _dt(*_I32), "indices"),
@@ -425,7 +522,7 @@ def embbag_baseline_touch_rows(batch, num_indices, weights, workspace, stream=No
 
 
 def embbag_status_read(d_status, stream=None) -> int:
-    return lib().embbag_status_read(_ptr(d_status, _dt(*_I32), "d_status"), _stream(stream))
+    return lib().embbag_status_read(_status_ptr(d_status), _stream(stream))
 
 
 __all__ = [n for n in dir() if n.startswith("embbag_") or n.startswith("EMBBAG_")] + [

@@ -82,3 +82,45 @@ def test_dtype_and_layout_checks():
     with pytest.raises(TypeError, match="pooled_out"):
         pk.embbag_forward_split_bf16_act([_FakeCuda(torch.zeros((10, 8), dtype=torch.int16))], 1,
                                          _FakeCuda(torch.zeros(4, dtype=torch.int32)), O, Y)
+
+
+def test_shape_checks_before_any_library_call():
+    """Sizes the C ABI takes on trust (it gets raw pointers) are checked here: a
+    narrower table, a short or long offsets array, activations of the wrong size
+    or mismatched split halves raise ValueError instead of reaching a kernel."""
+    f32 = lambda *shape: _FakeCuda(torch.zeros(shape))
+    i32 = lambda n: _FakeCuda(torch.zeros(n, dtype=torch.int32))
+    i16 = lambda *shape: _FakeCuda(torch.zeros(shape, dtype=torch.int16))
+    W = [f32(10, 8), f32(20, 8)]
+    I, O, Y = i32(6), i32(2 * 3 + 1), f32(2, 3, 8)
+    ws = _FakeCuda(torch.zeros(64, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="table 1"):
+        pk.embbag_forward([f32(10, 8), f32(20, 4)], 3, I, O, Y)
+    with pytest.raises(ValueError, match="table 0"):
+        pk.embbag_forward([f32(10, 8), f32(80)], 3, I, O, Y)
+    with pytest.raises(ValueError, match="offsets"):
+        pk.embbag_forward(W, 3, I, i32(6), Y)
+    with pytest.raises(ValueError, match="offsets"):
+        pk.embbag_backward_prepare((10, 20), 8, 3, I, i32(8), ws)
+    with pytest.raises(ValueError, match="pooled_out"):
+        pk.embbag_forward(W, 3, I, O, f32(2, 3, 4))
+    with pytest.raises(ValueError, match="grad_pooled"):
+        pk.embbag_backward_sgd(f32(2, 2, 8), 3, I, O, 0.1, W, ws)
+    with pytest.raises(ValueError, match="grad_pooled"):
+        pk.embbag_backward_apply_sgd(f32(1, 3, 8), 3, 6, 0.1, W, ws)
+    with pytest.raises(ValueError, match="per_sample_weights"):
+        pk.embbag_forward_pooled(W, 3, I, O, Y, f32(5))
+    with pytest.raises(ValueError, match="lo table 1"):
+        pk.embbag_backward_sgd_split_bf16(Y, 3, I, O, 0.1, [i16(10, 8), i16(20, 8)],
+                                          [i16(10, 8), i16(19, 8)], ws)
+    with pytest.raises(ValueError, match="lo tables"):
+        pk.embbag_backward_apply_sgd_split_bf16(Y, 3, 6, 0.1, [i16(10, 8), i16(20, 8)],
+                                                [i16(10, 8)], ws)
+    with pytest.raises(ValueError, match="seg_off"):
+        pk.embbag_dedup((10, 20), 3, I, O, i32(6), i32(6), i32(6), i32(6), i32(1), ws)
+    with pytest.raises(ValueError, match="lo"):
+        pk.embbag_split_fp32(f32(16), i16(16), i16(8))
+    with pytest.raises(ValueError, match="dW"):
+        pk.embbag_baseline_materialize(Y, 2, 3, 8, O, 6, f32(5, 8))
+    with pytest.raises(ValueError, match="d_status"):
+        pk.embbag_forward(W, 3, I, O, Y, i32(0))
