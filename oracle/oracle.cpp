@@ -95,6 +95,30 @@ int validate(int32_t T, int32_t B, int32_t E, const int64_t* rows, const int32_t
   return check_indices(T, B, rows, I, O);
 }
 
+// The forward's output buffer: null is an argument error unless there is
+// nothing to write (T*B = 0).  Checked after the sizes and the index and
+// offsets pointers and before the data, so that the status matches the
+// library's on the same arguments.
+int check_out(int32_t T, int32_t B, int32_t E, const int64_t* rows, const int32_t* I,
+              const int32_t* O, int64_t NS, const void* Y) {
+  int rc = check_args(T, B, E, rows, NS);
+  if (rc) return rc;
+  if (O == nullptr || (NS > 0 && I == nullptr)) return kErrInvalidArg;
+  if (int64_t(T) * B > 0 && Y == nullptr) return kErrInvalidArg;
+  return kOk;
+}
+
+// The backward's gradient: null is an argument error when there is a
+// look-up to update, checked before the data as the library does.
+int check_grad(int32_t T, int32_t B, int32_t E, const int64_t* rows, const int32_t* I,
+               const int32_t* O, int64_t NS, const void* dY) {
+  int rc = check_args(T, B, E, rows, NS);
+  if (rc) return rc;
+  if (O == nullptr || (NS > 0 && I == nullptr)) return kErrInvalidArg;
+  if (NS > 0 && dY == nullptr) return kErrInvalidArg;
+  return kOk;
+}
+
 inline float bits_to_float(uint32_t u) {
   float f;
   std::memcpy(&f, &u, 4);
@@ -123,7 +147,9 @@ struct RowReader {
 // W_t[I[s]], zero for an empty bag; bag k = t*B + b belongs to table t.
 int forward_impl(int32_t T, int32_t B, int32_t E, const int64_t* rows, const RowReader& W,
                  const int32_t* I, const int32_t* O, int64_t NS, float* Y) {
-  int rc = validate(T, B, E, rows, I, O, NS);
+  int rc = check_out(T, B, E, rows, I, O, NS, Y);
+  if (rc) return rc;
+  rc = validate(T, B, E, rows, I, O, NS);
   if (rc) return rc;
   std::vector<double> acc(E);
   for (int64_t k = 0; k < int64_t(T) * B; ++k) {
@@ -191,9 +217,10 @@ int table_of_key(const Dedup& d, uint32_t key) {
 template <class Apply>
 int backward_impl(const float* dY, int32_t T, int32_t B, int32_t E, const int64_t* rows,
                   const int32_t* I, const int32_t* O, int64_t NS, Apply apply) {
-  int rc = validate(T, B, E, rows, I, O, NS);
+  int rc = check_grad(T, B, E, rows, I, O, NS, dY);
   if (rc) return rc;
-  if (dY == nullptr && NS > 0) return kErrInvalidArg;
+  rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
   Dedup d;
   dedup_impl(T, B, rows, I, O, NS, d);
   std::vector<double> acc(E);
@@ -359,8 +386,10 @@ void oracle_bf16_widen(const uint16_t* h, float* out, int64_t n) {
 int oracle_forward_split_bf16_act(int32_t T, int32_t B, int32_t E, const int64_t* rows,
                                   const uint16_t* const* hi, const int32_t* I, const int32_t* O,
                                   int64_t NS, uint16_t* Y) {
-  if (hi == nullptr || Y == nullptr) return kErrInvalidArg;
-  int rc = validate(T, B, E, rows, I, O, NS);
+  if (hi == nullptr) return kErrInvalidArg;
+  int rc = check_out(T, B, E, rows, I, O, NS, Y);
+  if (rc) return rc;
+  rc = validate(T, B, E, rows, I, O, NS);
   if (rc) return rc;
   std::vector<float> y(size_t(T) * size_t(B) * size_t(E), 0.0f);
   rc = oracle_forward_split(T, B, E, rows, hi, I, O, NS, y.data());
@@ -376,9 +405,10 @@ int oracle_backward_sgd_split_bf16_act(const uint16_t* dY, int32_t T, int32_t B,
                                        uint16_t* const* lo, const int32_t* I, const int32_t* O,
                                        int64_t NS, float lr) {
   if (hi == nullptr || lo == nullptr) return kErrInvalidArg;
-  const int rc = validate(T, B, E, rows, I, O, NS);
+  int rc = check_grad(T, B, E, rows, I, O, NS, dY);
   if (rc) return rc;
-  if (dY == nullptr && NS > 0) return kErrInvalidArg;
+  rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
   const int64_t n = int64_t(T) * B * E;
   std::vector<float> g(static_cast<size_t>(n));
   if (n > 0 && dY != nullptr) oracle_bf16_widen(dY, g.data(), n);
@@ -393,7 +423,10 @@ int oracle_backward_sgd_split_bf16_act(const uint16_t* dY, int32_t T, int32_t B,
 int oracle_forward_literal(int32_t T, int32_t B, int32_t E, const int64_t* rows,
                            const float* const* W, const int32_t* I, const int32_t* O, int64_t NS,
                            float* Y) {
-  int rc = validate(T, B, E, rows, I, O, NS);
+  if (W == nullptr) return kErrInvalidArg;
+  int rc = check_out(T, B, E, rows, I, O, NS, Y);
+  if (rc) return rc;
+  rc = validate(T, B, E, rows, I, O, NS);
   if (rc) return rc;
   for (int64_t k = 0; k < int64_t(T) * B; ++k) {
     float* y = Y + k * E;
@@ -410,7 +443,10 @@ int oracle_forward_literal(int32_t T, int32_t B, int32_t E, const int64_t* rows,
 int oracle_backward_sgd_literal(const float* dY, int32_t T, int32_t B, int32_t E,
                                 const int64_t* rows, float* const* W, const int32_t* I,
                                 const int32_t* O, int64_t NS, float lr) {
-  int rc = validate(T, B, E, rows, I, O, NS);
+  if (W == nullptr) return kErrInvalidArg;
+  int rc = check_grad(T, B, E, rows, I, O, NS, dY);
+  if (rc) return rc;
+  rc = validate(T, B, E, rows, I, O, NS);
   if (rc) return rc;
   std::vector<float> dW(size_t(NS) * E, 0.0f);
   for (int64_t k = 0; k < int64_t(T) * B; ++k)
@@ -444,7 +480,9 @@ int oracle_forward_weighted(int32_t T, int32_t B, int32_t E, const int64_t* rows
                             const float* a, int32_t mode, float* Y) {
   if (W == nullptr || (mode != kPoolSum && mode != kPoolMean) || (mode == kPoolMean && a))
     return kErrInvalidArg;
-  int rc = validate(T, B, E, rows, I, O, NS);
+  int rc = check_out(T, B, E, rows, I, O, NS, Y);
+  if (rc) return rc;
+  rc = validate(T, B, E, rows, I, O, NS);
   if (rc) return rc;
   std::vector<double> acc(E);
   for (int64_t k = 0; k < int64_t(T) * B; ++k) {
@@ -467,9 +505,10 @@ int oracle_backward_sgd_weighted(const float* dY, int32_t T, int32_t B, int32_t 
                                  float lr) {
   if (W == nullptr || (mode != kPoolSum && mode != kPoolMean) || (mode == kPoolMean && a))
     return kErrInvalidArg;
-  int rc = validate(T, B, E, rows, I, O, NS);
+  int rc = check_grad(T, B, E, rows, I, O, NS, dY);
   if (rc) return rc;
-  if (dY == nullptr && NS > 0) return kErrInvalidArg;
+  rc = validate(T, B, E, rows, I, O, NS);
+  if (rc) return rc;
   Dedup d;
   dedup_impl(T, B, rows, I, O, NS, d);
   std::vector<double> acc(E);
