@@ -269,3 +269,46 @@ def test_large_split_full_size():
 
 def test_mlperf_split_full_size():
     _run_split("mlperf_split", grad_bf16=True)
+
+
+def test_maximum_lookup_count():
+    """The most look-ups one call accepts, 2^31 - 1 - 2^16 (the kernels index
+    look-ups in 32 bits and step up to 2^16 past the last one), through the
+    forward and the fused backward: every kernel's index arithmetic at its
+    limit.  One table of 1024 rows, E = 4, bags of 2048 look-ups (the last one
+    2047) with row s mod 1024, so every full bag reads each row twice.  Weights
+    are small integers and gradients binary fractions, so every expected value
+    has a closed form that is exact in FP32: each pooled output and every
+    updated row must match bit for bit, and no pooled row may stay unwritten."""
+    NS = 2 ** 31 - 1 - 2 ** 16
+    P, M, E, lr = 2048, 1024, 4, 0.5
+    B = (NS + P - 1) // P
+    log(f"[full] maximum look-up count: NS={NS}, B={B}, M={M}, E={E}")
+    Wh = ((np.arange(M)[:, None] * 7 + np.arange(E)[None, :] * 3) % 17 - 8).astype(np.float32)
+    W = torch.from_numpy(Wh).to(DEV)
+    I = torch.arange(NS, dtype=torch.int32, device=DEV).bitwise_and_(M - 1)
+    O = torch.clamp(torch.arange(B + 1, dtype=torch.int64, device=DEV) * P, max=NS).to(torch.int32)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    Y = torch.full((1, B, E), float("nan"), dtype=torch.float32, device=DEV)
+    pk.check(pk.embbag_forward([W], B, I, O, Y, status), "forward")
+    pk.check(pk.embbag_status_read(status), "forward status")
+    full = 2.0 * Wh.astype(np.float64).sum(0)
+    Yexp = np.broadcast_to(full, (B, E)).copy()
+    Yexp[B - 1] -= Wh[M - 1]  # the last bag misses row 1023's second read
+    Yg = Y.cpu().numpy().reshape(B, E)
+    assert bits_equal(Yg, Yexp.astype(np.float32)), "pooled outputs"
+
+    k = np.arange(B, dtype=np.float64)
+    dY = (((k % 5) - 2) * 2.0 ** -6)[:, None] + np.arange(E)[None, :] * 2.0 ** -8
+    dYd = torch.from_numpy(dY.astype(np.float32)).reshape(1, B, E).to(DEV)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(1, B, NS, E), dtype=torch.uint8,
+                     device=DEV)
+    pk.check(pk.embbag_backward_sgd(dYd, B, I, O, lr, [W], ws, status), "backward_sgd")
+    pk.check(pk.embbag_status_read(status), "backward status")
+    mult = np.full(M, 2.0)
+    mult[M - 1] = 1.0  # row 1023 is read once by the last bag
+    G = 2.0 * dY[:B - 1].sum(0)[None, :] + mult[:, None] * dY[B - 1][None, :]
+    Wexp = (Wh.astype(np.float64) - lr * G).astype(np.float32)
+    assert bits_equal(W.cpu().numpy(), Wexp), "updated rows"
+    del I, O, Y, ws
+    torch.cuda.empty_cache()
