@@ -148,8 +148,6 @@ uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows, int 
 
 BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
                           bool for_dedup) {
-  (void)T;
-  (void)B;
   BwdLayout L{};
   L.ns = NS;
   // As few passes as digits of at most 10 bits allow, the bits spread evenly
@@ -171,7 +169,12 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
          (NS + int64_t(kBlock) * L.ipt - 1) / (int64_t(kBlock) * L.ipt) < 512)
     L.ipt /= 2;
   L.ntiles = (NS + int64_t(kBlock) * L.ipt - 1) / (int64_t(kBlock) * L.ipt);
-  L.nkeyblocks = L.ntiles > 0 ? L.ntiles : 1;
+  // Key-build blocks: one per tile, and at least one per kOffsetsPerBlock
+  // offsets, which they validate (with few look-ups in many bags, one block
+  // per tile would leave all the offsets to a handful of blocks).
+  const int64_t vblocks = (int64_t(T) * B + 1 + kOffsetsPerBlock - 1) / kOffsetsPerBlock;
+  L.nkeyblocks = L.ntiles > vblocks ? L.ntiles : vblocks;
+  if (L.nkeyblocks < 1) L.nkeyblocks = 1;
   // Chunk of the segmented reduce: at least 128 look-ups per wavefront (a
   // wavefront walks one chunk per row group), growing to at most 1024 while
   // at least ~32K wavefronts remain (Large: 256 look-ups, 51K wavefronts;

@@ -23,6 +23,7 @@ constexpr int kMaxRadixBits = 10;
 constexpr int kMaxRadix = 1 << kMaxRadixBits;
 constexpr int kMaxItemsPerThread = 16;  // radix tile: kBlock * (4, 8 or 16) keys
 constexpr int kCarryGroup = 16;  // chunks per pre-summed group of carries
+constexpr int64_t kOffsetsPerBlock = 16384;  // offsets a key-build block validates, at most
 
 // Sentinel for "no key": keys are < 2^31 because sum(M_t) < 2^31.
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;

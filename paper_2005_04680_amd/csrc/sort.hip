@@ -109,7 +109,8 @@ __global__ __launch_bounds__(kBlock) void build_keys(
   // Offsets: O[0] == 0, O non-decreasing, O[TB] == NS, all within [0, NS].
   // kOq offsets per thread are requested before any is checked (with one
   // look-up per bag a block checks thousands of them).
-  const int kb0 = blk * vb, kb1 = min(kb0 + vb, TB + 1);
+  // 64-bit: with both NS and T*B near 2^31, blk * vb passes 2^31 - 1.
+  const int64_t kb0 = int64_t(blk) * vb, kb1 = min(kb0 + vb, int64_t(TB) + 1);
   for (int64_t k0 = kb0 + tid; k0 < kb1; k0 += kBlock * kOq) {
     int oa[kOq], ob[kOq];
 #pragma unroll
@@ -256,8 +257,14 @@ __global__ __launch_bounds__(kBlock) void radix_scan(uint32_t* __restrict__ hist
   if (int(blockIdx.x) == radix / 4) {
     if (tid == 0) lerr = 0;
     __syncthreads();
-    int e = 0;
-    for (int i = tid; i < nparts; i += kBlock) e = min(e, parts[i]);
+    int e = 0;  // kOq words per thread requested before any is folded
+    for (int i0 = tid; i0 < nparts; i0 += kBlock * kOq) {
+      int v[kOq];
+#pragma unroll
+      for (int q = 0; q < kOq; ++q) v[q] = i0 + q * kBlock < nparts ? parts[i0 + q * kBlock] : 0;
+#pragma unroll
+      for (int q = 0; q < kOq; ++q) e = min(e, v[q]);
+    }
     if (e != 0) atomicMin(&lerr, e);
     __syncthreads();
     if (tid == 0) {
@@ -574,7 +581,7 @@ hipError_t sort_passes(const TableDesc& d, int32_t B, const int32_t* I, const in
   int32_t* parts = reinterpret_cast<int32_t*>(ws + L.off_parts);
   int32_t* flags = reinterpret_cast<int32_t*>(ws + L.off_flags);
   const int nkb = int(L.nkeyblocks);
-  const int vb = (TB + 1 + nkb - 1) / nkb;
+  const int vb = int((int64_t(TB) + 1 + nkb - 1) / nkb);
   const int ntiles = int(L.ntiles);
   const float inv_b = B > 0 ? 1.0f / float(B) : 0.0f;
   float* va = reinterpret_cast<float*>(ws + L.off_va);

@@ -312,3 +312,60 @@ def test_maximum_lookup_count():
     assert bits_equal(W.cpu().numpy(), Wexp), "updated rows"
     del I, O, Y, ws
     torch.cuda.empty_cache()
+
+
+def test_maximum_lookups_and_bags_together():
+    """Both limits in one call: 2^31 - 1 - 2^16 look-ups and T*B + 1 = 2^31 - 1
+    offsets (2 tables of 2^30 - 1 bags, one look-up per bag, the last 65535
+    bags empty).  This is where the key build's validation slices pass 2^31
+    offsets.  Look-up s of table t reads row (s - t*B) mod 768; B and 768 are
+    multiples of 3, so gradients that depend on the bag index mod 3 give each
+    row a sum with a closed form.  Weights are small integers and gradients
+    binary fractions: every pooled output (compared on the device, slice by
+    slice) and every updated row must match bit for bit.  About 140 GB of
+    device memory."""
+    T, B, M, E, lr = 2, 2 ** 30 - 1, 768, 4, 0.5
+    NS, TB = 2 ** 31 - 1 - 2 ** 16, 2 * (2 ** 30 - 1)
+    log(f"[full] maximum look-ups and bags: NS={NS}, T*B+1={TB + 1}, M={M}, E={E}")
+    rng = np.random.default_rng(31)
+    Wh = rng.integers(-8, 9, (T, M, E)).astype(np.float32)
+    W = [torch.from_numpy(Wh[t]).to(DEV) for t in range(T)]
+    I = torch.arange(NS, dtype=torch.int32, device=DEV)
+    I[B:] -= B
+    I.remainder_(M)
+    O = torch.arange(TB + 1, dtype=torch.int32, device=DEV).clamp_(max=NS)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    Y = torch.full((T, B, E), float("nan"), dtype=torch.float32, device=DEV)
+    pk.check(pk.embbag_forward(W, B, I, O, Y, status), "forward")
+    pk.check(pk.embbag_status_read(status), "forward status")
+    Wd = torch.from_numpy(Wh).to(DEV)
+    Yf = Y.view(TB, E)
+    step = 1 << 26
+    for lo in range(0, TB, step):
+        k = torch.arange(lo, min(lo + step, TB), dtype=torch.int64, device=DEV)
+        t = torch.div(k, B, rounding_mode="floor")
+        exp = Wd[t, (k - t * B) % M]
+        exp[k >= NS] = 0.0
+        got = Yf[lo:lo + k.numel()]
+        assert torch.equal(got.view(torch.int32), exp.view(torch.int32)), f"pooled outputs in [{lo}, +{k.numel()})"
+    del Y, Yf
+
+    dY = torch.empty((T, B, E), dtype=torch.float32, device=DEV)
+    dYf = dY.view(TB, E)
+    col = torch.arange(E, dtype=torch.float32, device=DEV) * 2.0 ** -6
+    for lo in range(0, TB, step):
+        k = torch.arange(lo, min(lo + step, TB), dtype=torch.int64, device=DEV)
+        dYf[lo:lo + k.numel()] = (((k % 3) - 1).to(torch.float32) * 2.0 ** -4)[:, None] + col[None, :]
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8,
+                     device=DEV)
+    pk.check(pk.embbag_backward_sgd(dY, B, I, O, lr, W, ws, status), "backward_sgd")
+    pk.check(pk.embbag_status_read(status), "backward status")
+    n = (B, NS - B)  # look-ups of each table
+    r = np.arange(M)
+    for t in range(T):
+        cnt = np.where(r < n[t], (n[t] - r + M - 1) // M, 0).astype(np.float64)
+        G = cnt[:, None] * ((((r % 3) - 1) * 2.0 ** -4)[:, None] + np.arange(E)[None, :] * 2.0 ** -6)
+        Wexp = (Wh[t].astype(np.float64) - lr * G).astype(np.float32)
+        assert bits_equal(W[t].cpu().numpy(), Wexp), f"updated rows of table {t}"
+    del I, O, dY, dYf, ws
+    torch.cuda.empty_cache()
