@@ -11,6 +11,10 @@ sampled untouched rows per table group (bit-identical), the full integer
 dedup (bit-exact), and the device fill against the host generator.  The
 split-storage runs (Section VII) check FP32 and BF16 pooled outputs and the
 update driven by an FP32 (Large-shaped) or BF16 (MLPerf-style) gradient.
+
+Two more runs go to the size limits of one call (2^31 - 1 - 2^16 look-ups,
+then also T*B + 1 = 2^31 - 1 offsets) with inputs whose every expected value
+has an exact closed form, checked bit for bit.
 """
 import numpy as np
 import pytest
