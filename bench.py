@@ -124,7 +124,19 @@ def host_cpu():
                     break
     except OSError:
         pass
-    return f"{model}, {os.cpu_count()} logical CPUs"
+    return f"{model}, {os.cpu_count()} logical CPUs, {host_ram_gb()} GB RAM"
+
+
+def host_ram_gb():
+    """Installed host memory in GB (MemTotal of /proc/meminfo), or None."""
+    try:
+        with open("/proc/meminfo") as f:
+            for line in f:
+                if line.startswith("MemTotal:"):
+                    return round(int(line.split()[1]) * 1024 / 1e9, 1)
+    except (OSError, ValueError, IndexError):
+        pass
+    return None
 
 
 def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
