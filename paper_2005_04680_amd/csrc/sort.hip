@@ -9,7 +9,7 @@
 // the key width allows: 3 for 27- or 28-bit keys): a per-tile digit
 // histogram, a scan per digit over the tiles, and a scatter in which every
 // tile (1024, 2048 or 4096 keys: the largest that still gives two tiles per
-// compute unit) is ranked in LDS (wavefront ballots give each lane its rank
+// compute unit and two keys per digit value) is ranked in LDS (wavefront ballots give each lane its rank
 // among equal digits) and written out in digit order, so that the global
 // stores form runs of consecutive addresses.  No kernel waits on another
 // workgroup.
