@@ -9,10 +9,10 @@
 // the key width allows: 3 for 27- or 28-bit keys): a per-tile digit
 // histogram, a scan per digit over the tiles, and a scatter in which every
 // tile (1024, 2048 or 4096 keys: the largest that still gives two tiles per
-// compute unit and two keys per digit value) is ranked in LDS (wavefront ballots give each lane its rank
-// among equal digits) and written out in digit order, so that the global
-// stores form runs of consecutive addresses.  No kernel waits on another
-// workgroup.
+// compute unit and two keys per digit value) is ranked in LDS (wavefront
+// ballots give each lane its rank among equal digits) and written out in
+// digit order, so that the global stores form runs of consecutive addresses.
+// No kernel waits on another workgroup.
 #include "common.hpp"
 
 namespace embbag {
@@ -63,7 +63,8 @@ struct Radix {
   static constexpr int DPT = R > kBlock ? R / kBlock : 1;
 };
 
-// Offsets read per thread before the first is used, in build_keys.
+// Loads per thread requested before the first is used (the offsets in
+// build_keys, the status words in the first scan).
 constexpr int kOq = 8;
 
 // Bags, keys and the first digit's histogram for one tile; offsets checks for
