@@ -211,13 +211,13 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
 
 
 def time_graph(torch, batches, prep, fwd, apply, K, warmup):
-    """The step (prepare, forward, apply) captured once per batch as a HIP graph;
+    """The step (forward, prepare, apply) captured once per batch as a HIP graph;
     K replays rotating over the batches, timed with events on the replay stream."""
     graphs = []
     for bt in batches:
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            rcs = (prep(bt), fwd(bt), apply(bt))
+            rcs = (fwd(bt), prep(bt), apply(bt))
         assert rcs == (0, 0, 0), rcs
         graphs.append(g)
     stream = torch.cuda.current_stream()
@@ -444,18 +444,22 @@ def main():
     side = torch.cuda.Stream(device=dev) if args.overlap_prepare else main
 
     def step(bt, prev, evs=None):
-        """One step: prepare (on `side`, after `prev`), forward, apply; returns
+        """One step: forward, prepare (on `side`, after `prev`), apply; returns
         the event after the apply.  `evs` (six timing events) bracket the calls."""
         e_f0, e_f1, e_p0, e_p1, e_a0, e_a1 = evs if evs is not None else tuple(
             torch.cuda.Event(enable_timing=False) for _ in range(6))
+        # Forward first, as in a training step; the index phase needs only the
+        # indices and offsets, so it follows (or, with --overlap-prepare, runs
+        # beside) the forward, and its sorted look-ups are then still in the
+        # MALL when the apply reads them.
+        e_f0.record(main)
+        pk.check(fwd(bt), "forward")
+        e_f1.record(main)
         side.wait_event(prev)
         with torch.cuda.stream(side):
             e_p0.record(side)
             pk.check(prep(bt), "prepare")
             e_p1.record(side)
-        e_f0.record(main)
-        pk.check(fwd(bt), "forward")
-        e_f1.record(main)
         main.wait_event(e_p1)
         e_a0.record(main)
         pk.check(apply(bt), "apply")
