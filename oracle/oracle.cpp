@@ -43,10 +43,10 @@ constexpr int kErrIndexRange = -3;
 constexpr int kErrOffsets = -4;
 
 constexpr int64_t kInt32Max = 2147483647;
-// The largest look-up count the library accepts: 2^31 - 1 - 2^16 (it indexes
-// look-ups in 32 bits with headroom), rejected alike here so that both sides
-// return the same status on the same arguments.
-constexpr int64_t kMaxIndices = kInt32Max - 65536;
+// Indices and offsets are int32 (Algorithm 1's I[NS] and O[N+1], read as
+// 32-bit integers), so a call holds at most 2^31 - 1 look-ups; more is an
+// argument error.
+constexpr int64_t kMaxIndices = kInt32Max;
 
 // Argument checks, first in the fixed validation order.
 int check_args(int32_t T, int32_t B, int32_t E, const int64_t* rows, int64_t NS) {

@@ -289,6 +289,98 @@ def test_literal_order_within_tolerance(oracle):
     del rng
 
 
+def _fp32_forward_in_order(W, batch, I, O):
+    """Algorithm 1 with an FP32 accumulator, look-ups in increasing s: numpy
+    float32 additions, one look-up at a time (IEEE single rounding each step)."""
+    T, E = len(W), W[0].shape[1]
+    Y = np.zeros((T, batch, E), np.float32)
+    for k in range(T * batch):
+        t, b = divmod(k, batch)
+        y = np.zeros(E, np.float32)
+        for s in range(O[k], O[k + 1]):
+            y = (y + W[t][I[s]]).astype(np.float32)
+        Y[t, b] = y
+    return Y
+
+
+def _fp32_update_in_order(G, batch, I, O, lr, W, reverse=False):
+    """Algorithm 2 then Algorithm 3 applied one look-up at a time in increasing
+    s, in FP32: w <- w + fl(alpha * dW[s]) with alpha = -lr (Section III-A;
+    within one row this is also Algorithm 4's order).  `reverse` walks the
+    look-ups from the last one instead (only to show that order matters)."""
+    T, E = len(W), W[0].shape[1]
+    alpha = np.float32(-lr)
+    out = [w.copy() for w in W]
+    ks = range(T * batch - 1, -1, -1) if reverse else range(T * batch)
+    for k in ks:
+        t, b = divmod(k, batch)
+        g = G[t, b].astype(np.float32)
+        ss = range(O[k], O[k + 1])
+        for s in (reversed(ss) if reverse else ss):
+            step = (alpha * g).astype(np.float32)
+            out[t][I[s]] = (out[t][I[s]] + step).astype(np.float32)
+    return out
+
+
+def test_literal_readings_absorb_in_order(oracle):
+    """Worked example where FP32 order decides the bits.  Forward: a bag reads
+    a row of 1.0 and then four rows of 2^-24 (half an ulp of 1): each addition
+    ties and rounds back to 1.0, so Algorithm 1 in FP32 gives exactly 1.0,
+    while the small rows first (reversed order) give 1 + 2^-22 and an FP64
+    accumulator 1 + 2^-22 too.  Update: a zero row receives a step of +1 and
+    then four steps of +2^-25 (lr = 1): sequential FP32 keeps 1.0 (each step is
+    a quarter ulp), reversed order or an FP64 sum gives 1 + 2^-23."""
+    E = 4
+    W = [np.array([[1.0] * E, [2.0 ** -24] * E, [0.0] * E], np.float32)]
+    I = np.array([0, 1, 1, 1, 1], np.int32)
+    O = np.array([0, 5], np.int32)
+    rc, Y = oracle.forward(W, 1, I, O, literal=True)
+    assert rc == oracle.OK
+    assert np.array_equal(Y[0, 0].view(np.uint32), np.full(E, np.float32(1.0)).view(np.uint32))
+    rc, Yd = oracle.forward(W, 1, I, O)  # the FP64 definition: exact sum, rounded once
+    assert rc == oracle.OK and np.all(Yd[0, 0] == np.float32(1.0 + 4 * 2.0 ** -24))
+    # update: bag 0 = [row 2], bag 1 = [row 2] x 4; dY chosen so that -lr*g is
+    # +1 for bag 0 and +2^-25 for bag 1
+    I = np.array([2, 2, 2, 2, 2], np.int32)
+    O = np.array([0, 1, 5], np.int32)
+    G = np.array([[[-1.0] * E, [-(2.0 ** -25)] * E]], np.float32)
+    Wl = [W[0].copy()]
+    assert oracle.backward_sgd(G, 2, I, O, 1.0, Wl, literal=True) == oracle.OK
+    assert np.array_equal(Wl[0][2], np.full(E, np.float32(1.0)))
+    assert np.array_equal(Wl[0][:2], W[0][:2])
+    Wd = [W[0].copy()]
+    assert oracle.backward_sgd(G, 2, I, O, 1.0, Wd) == oracle.OK
+    assert np.all(Wd[0][2] == np.float32(1.0 + 2.0 ** -23))
+
+
+@pytest.mark.parametrize("seed", [21, 22, 23])
+def test_literal_readings_follow_fp32_order(oracle, seed):
+    """The literal readings are Algorithm 1 and Algorithm 3 in FP32, look-ups in
+    increasing s: bit for bit what a numpy float32 loop in that order gives,
+    on values whose magnitudes span ten decades (so sums depend on order:
+    the test also checks that reversed order changes some bits)."""
+    rng = np.random.default_rng(seed)
+    rows, dim, batch = (40, 9), 8, 12
+    mag = lambda *sh: (10.0 ** rng.uniform(-8, 2, sh)) * rng.choice([-1.0, 1.0], sh)
+    W = [mag(m, dim).astype(np.float32) for m in rows]
+    I, O = random_bags(rng, rows, batch, 24, 0.1, 0.5)
+    G = mag(len(rows), batch, dim).astype(np.float32)
+    lr = 0.37
+    rc, Y = oracle.forward(W, batch, I, O, literal=True)
+    assert rc == oracle.OK
+    Yexp = _fp32_forward_in_order(W, batch, I, O)
+    assert np.array_equal(Y.view(np.uint32), Yexp.view(np.uint32))
+    Irev = np.concatenate([I[O[k]:O[k + 1]][::-1] for k in range(len(O) - 1)]).astype(np.int32)
+    assert not np.array_equal(_fp32_forward_in_order(W, batch, Irev, O), Yexp)
+    Wl = [w.copy() for w in W]
+    assert oracle.backward_sgd(G, batch, I, O, lr, Wl, literal=True) == oracle.OK
+    Wexp = _fp32_update_in_order(G, batch, I, O, lr, W)
+    for a, b in zip(Wl, Wexp):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    Wrev = _fp32_update_in_order(G, batch, I, O, lr, W, reverse=True)
+    assert any(not np.array_equal(a, b) for a, b in zip(Wrev, Wexp))
+
+
 # ----------------------------------------------------------------------------
 # validation and status codes
 # ----------------------------------------------------------------------------
@@ -302,9 +394,11 @@ def test_status_codes(oracle):
     assert oracle.validate(rows, 8, -1, I, O) == oracle.ERR_INVALID_ARG
     assert oracle.validate(rows, 8, 2, I, O, num_tables=0) == oracle.ERR_INVALID_ARG
     assert oracle.validate((10, 0), 8, 2, I, O) == oracle.ERR_INVALID_ARG
-    # more look-ups than the library accepts (2^31 - 1 - 2^16): rejected with the
-    # arguments, before the arrays are read
-    assert oracle.validate(rows, 8, 2, I, O, num_indices=2 ** 31 - 2 ** 16) == oracle.ERR_INVALID_ARG
+    # indices and offsets are int32: more than 2^31 - 1 look-ups is an argument
+    # error, found before the arrays are read; 2^31 - 1 itself passes the
+    # argument checks (here the offsets then disagree with it)
+    assert oracle.validate(rows, 8, 2, I, O, num_indices=2 ** 31) == oracle.ERR_INVALID_ARG
+    assert oracle.validate(rows, 8, 2, I, O, num_indices=2 ** 31 - 1) == oracle.ERR_OFFSETS
     bad = O.copy(); bad[0] = 1
     assert oracle.validate(rows, 8, 2, I, bad) == oracle.ERR_OFFSETS
     bad = np.array([0, 2, 1, 3, 4], np.int32)

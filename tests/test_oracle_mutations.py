@@ -85,6 +85,44 @@ MUTATIONS = {
     "weighted_bwd_ignores_weights": ("      if (a) c = double(a[s]);\n", ""),
     "mean_bwd_not_divided": ("      if (mode == kPoolMean) c = 1.0 / double(O[k + 1] - O[k]);\n", ""),
     "mean_fwd_wrong_count": ("acc[e] / double(n)", "acc[e] / double(n + 1)"),
+    # the literal FP32 readings (Algorithm 1; Algorithm 3 one look-up at a time)
+    "literal_fwd_reversed": (
+        "    for (int64_t s = O[k]; s < O[k + 1]; ++s)\n"
+        "      for (int e = 0; e < E; ++e) y[e] += W[k / B][int64_t(I[s]) * E + e];",
+        "    for (int64_t s = O[k + 1] - 1; s >= O[k]; --s)\n"
+        "      for (int e = 0; e < E; ++e) y[e] += W[k / B][int64_t(I[s]) * E + e];"),
+    "literal_fwd_fp64_accumulator": (
+        "    for (int e = 0; e < E; ++e) y[e] = 0.0f;\n"
+        "    for (int64_t s = O[k]; s < O[k + 1]; ++s)\n"
+        "      for (int e = 0; e < E; ++e) y[e] += W[k / B][int64_t(I[s]) * E + e];",
+        "    std::vector<double> a(E, 0.0);\n"
+        "    for (int64_t s = O[k]; s < O[k + 1]; ++s)\n"
+        "      for (int e = 0; e < E; ++e) a[e] += W[k / B][int64_t(I[s]) * E + e];\n"
+        "    for (int e = 0; e < E; ++e) y[e] = float(a[e]);"),
+    "literal_update_reversed": (
+        "  const float alpha = -lr;\n  for (int64_t k = 0; k < int64_t(T) * B; ++k)\n"
+        "    for (int64_t i = O[k]; i < O[k + 1]; ++i) {",
+        "  const float alpha = -lr;\n  for (int64_t k = int64_t(T) * B - 1; k >= 0; --k)\n"
+        "    for (int64_t i = O[k + 1] - 1; i >= O[k]; --i) {"),
+    "literal_update_fp64_accumulator": (
+        "  const float alpha = -lr;\n"
+        "  for (int64_t k = 0; k < int64_t(T) * B; ++k)\n"
+        "    for (int64_t i = O[k]; i < O[k + 1]; ++i) {\n"
+        "      float* w = W[k / B] + int64_t(I[i]) * E;\n"
+        "      for (int e = 0; e < E; ++e) {\n"
+        "        const float step = alpha * dW[i * E + e];\n"
+        "        w[e] = w[e] + step;\n"
+        "      }\n"
+        "    }",
+        "  const float alpha = -lr;\n"
+        "  std::vector<std::vector<double>> acc(T);\n"
+        "  for (int t = 0; t < T; ++t) acc[t].assign(W[t], W[t] + rows[t] * E);\n"
+        "  for (int64_t k = 0; k < int64_t(T) * B; ++k)\n"
+        "    for (int64_t i = O[k]; i < O[k + 1]; ++i)\n"
+        "      for (int e = 0; e < E; ++e)\n"
+        "        acc[k / B][int64_t(I[i]) * E + e] += double(alpha) * dW[i * E + e];\n"
+        "  for (int t = 0; t < T; ++t)\n"
+        "    for (int64_t j = 0; j < rows[t] * E; ++j) W[t][j] = float(acc[t][j]);"),
 }
 
 
