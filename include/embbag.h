@@ -23,8 +23,7 @@
  * Bags.  `batch` = B bags per table.  Bag k = t*B + b reads
  *   indices[offsets[k] .. offsets[k+1]) (half-open), rows of table t.
  *   `indices`: device int32 [num_indices], table-local rows; num_indices <=
- *   2^31 - 1 - 2^16 (look-ups are indexed in 32 bits, with headroom for the
- *   last radix tile and reduce chunk).
+ *   2^31 - 1 (indices and offsets are int32).
  *   `offsets`: device int32 [T*B + 1], offsets[0] == 0, non-decreasing,
  *   offsets[T*B] == num_indices.  (Algorithm 1's header swaps the two sizes;
  *   its loops read O[n] and O[n+1].)  A row may repeat within and across
@@ -92,7 +91,7 @@ typedef struct {
 /* Forward, Algorithm 1 (sum pooling): for every bag k = t*B + b,
  *   pooled_out[t][b][:] = sum over s in [offsets[k], offsets[k+1]) of
  *                         weights[t][indices[s]][:]        (+0.0 if empty).
- * FP32 accumulation in look-up order within each lane's partial sums.
+ * Each bag is summed in FP64 in look-up order and rounded once to FP32.
  * `d_status` (device int32, nullable) receives data errors as described in
  * the header comment. */
 int embbag_forward(const embbag_tables_t* tables, int32_t batch, const int32_t* indices,
@@ -244,7 +243,10 @@ int embbag_combine_fp32(const uint16_t* hi, const uint16_t* lo, float* w, int64_
 /* Bytes of device workspace embbag_dedup needs (256-byte aligned). */
 size_t embbag_dedup_workspace_bytes(int32_t num_tables, int32_t batch, int64_t num_indices);
 
-/* Integer work of the backward, exposed for bit-exact checking:
+/* Integer work of the backward, exposed for bit-exact checking.  Algorithm 2's
+ * loop over bags n and look-ups s gives every look-up its bag; the look-ups
+ * grouped by row are what Algorithm 3 needs to add all of a row's gradients
+ * and Algorithm 4 to give each row a single writer (Section III-A):
  *   key[s] = rowbase[t] + indices[s] (rowbase = exclusive prefix sum of rows),
  *   bag[s] = k for offsets[k] <= s < offsets[k+1];
  *   (sorted_keys, sorted_bags)[NS] = (key, bag) stably sorted by key (ties in

@@ -9,10 +9,11 @@ using namespace embbag;
 namespace {
 
 constexpr int64_t kInt32Max = 2147483647;
-// Look-ups per call: the kernels index look-ups in 32 bits and step up to a
-// radix tile (4096) or a reduce chunk past the last one, so 2^16 of headroom
-// below 2^31 keeps every such sum in range.
-constexpr int64_t kMaxIndices = kInt32Max - 65536;
+// Look-ups per call: indices and offsets are int32 (Algorithm 1's I[NS] and
+// O[N+1]), so at most 2^31 - 1.  The kernels hold look-up positions in
+// unsigned 32-bit arithmetic, where stepping a tile or a chunk past the last
+// look-up still stays below 2^32.
+constexpr int64_t kMaxIndices = kInt32Max;
 constexpr size_t kWsAlign = 256;
 
 bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
@@ -90,7 +91,7 @@ int prepare_common(const TableDesc& d, int32_t B, const int32_t* I, const int32_
   const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
   if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
   return hip_status(launch_sort(d, B, I, O, NS, L, static_cast<char*>(ws), d_status,
-                                phase_token(d.num_tables, B, NS, total, mode),
+                                phase_token(d.num_tables, B, NS, d.dim, total, mode),
                                 mode == kPoolWeighted ? weights : nullptr, st));
 }
 
@@ -105,8 +106,8 @@ int apply_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16, i
   const BwdLayout L = backward_layout(d.num_tables, B, NS, d.dim, total, false);
   if (ws == nullptr || !aligned(ws, kWsAlign) || ws_bytes < L.total) return EMBBAG_ERR_WORKSPACE;
   return hip_status(launch_segment_sgd(d, split, B, dY, dy_bf16, lr, L, static_cast<char*>(ws),
-                                       phase_token(d.num_tables, B, NS, total, pool.mode), pool,
-                                       st));
+                                       phase_token(d.num_tables, B, NS, d.dim, total, pool.mode),
+                                       pool, st));
 }
 
 int backward_common(const TableDesc& d, bool split, const void* dY, bool dy_bf16, int32_t B,
@@ -133,12 +134,14 @@ int split_desc(const embbag_split_tables_t* tables, bool need_lo, TableDesc* d) 
 
 namespace embbag {
 
-uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows, int mode) {
-  // A weighted prepare also sorts the weights along; the others do not.
+uint32_t phase_token(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
+                     int mode) {
+  // A weighted prepare also sorts the weights along; the others do not.  E
+  // sizes the carry regions, which the sorted weights follow.
   const uint64_t payload = mode == kPoolWeighted ? 1u : 0u;
   uint64_t h = 0x243F6A8885A308D3ull;
   for (uint64_t v : {uint64_t(uint32_t(T)), uint64_t(uint32_t(B)), uint64_t(NS),
-                     uint64_t(total_rows), payload}) {
+                     uint64_t(uint32_t(E)), uint64_t(total_rows), payload}) {
     h ^= v + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
     h *= 0xBF58476D1CE4E5B9ull;
   }
@@ -471,7 +474,8 @@ int embbag_dedup(int32_t num_tables, const int64_t* rows, int32_t batch, const i
     return EMBBAG_ERR_WORKSPACE;
   char* w = static_cast<char*>(workspace);
   if (launch_sort(d, batch, indices, offsets, num_indices, L, w, d_status,
-                  phase_token(num_tables, batch, num_indices, d.rowbase[num_tables], kPoolPlain),
+                  phase_token(num_tables, batch, num_indices, 4, d.rowbase[num_tables],
+                              kPoolPlain),
                   nullptr, stream) != hipSuccess)
     return EMBBAG_ERR_HIP;
   return hip_status(launch_unique(sorted_buffer(L, w), L, w, sorted_keys, sorted_bags,
@@ -558,8 +562,8 @@ int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_
   if (workspace == nullptr || !aligned(workspace, kWsAlign) || workspace_bytes < L.total)
     return EMBBAG_ERR_WORKSPACE;
   return hip_status(launch_touch_rows(d, batch, L, static_cast<char*>(workspace),
-                                      phase_token(d.num_tables, batch, num_indices, total,
-                                                  kPoolPlain),
+                                      phase_token(d.num_tables, batch, num_indices, d.dim,
+                                                  total, kPoolPlain),
                                       stream));
 }
 

@@ -124,19 +124,20 @@ __global__ __launch_bounds__(kWave) void owner_update_kernel(TableDesc d,
   const uint32_t khi = uint32_t(K * uint64_t(j + 1) / uint64_t(owners));
   const float alpha = -lr;
   int t = 0;
-  for (int base = 0; base < NS; base += kWave) {
-    const int s = base + lane;
+  // unsigned: with num_indices = 2^31 - 1 the last window runs past it
+  for (uint32_t base = 0; base < uint32_t(NS); base += kWave) {
+    const uint32_t s = base + lane;
     // table of look-up s: tables own contiguous look-up ranges
     int tl = t;
-    while (tl + 1 < T && s >= O[(tl + 1) * B]) ++tl;
-    const int idx = s < NS ? I[s] : -1;
-    const bool ok = s < NS && uint32_t(idx) < d.rows[tl];
+    while (tl + 1 < T && int64_t(s) >= O[(tl + 1) * B]) ++tl;
+    const int idx = s < uint32_t(NS) ? I[s] : -1;
+    const bool ok = s < uint32_t(NS) && uint32_t(idx) < d.rows[tl];
     const uint32_t key = ok ? d.rowbase[tl] + uint32_t(idx) : 0u;
     uint64_t mine = __builtin_amdgcn_ballot_w64(ok && key >= klo && key < khi);
     while (mine) {
       const int l = __builtin_ctzll(mine);
       mine &= mine - 1;
-      const int so = base + l;
+      const uint32_t so = base + l;
       const int to = __builtin_amdgcn_readlane(tl, l);
       const uint32_t ro = uint32_t(__builtin_amdgcn_readlane(idx, l));
       float* w = static_cast<float*>(d.w[to]) + size_t(ro) * E;
@@ -183,9 +184,11 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
   const int blk = int(logical_block(in_order != 0));
   const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
-  const int lo = chunk * C, hi = min(lo + C, NS);
+  // unsigned: with num_indices = 2^31 - 1 the last group runs past it
+  const uint32_t lo = uint32_t(chunk) * uint32_t(C);
+  const uint32_t hi = min(lo + uint32_t(C), uint32_t(NS));
   uint32_t prev = lo > 0 ? key_of(sorted[lo - 1]) : kNoKey;
-  for (int s = lo; s < hi; s += H) {
+  for (uint32_t s = lo; s < hi; s += H) {
     bool head[H];
     int tb[H];
     uint32_t row[H];

@@ -174,8 +174,10 @@ BwdLayout backward_layout(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t 
                           bool for_dedup);
 
 // Stamp the sort phase leaves in the workspace for the apply phase: a hash of
-// the sizes the sorted look-ups belong to and of their payload (never 0).
-uint32_t phase_token(int32_t T, int32_t B, int64_t NS, uint32_t total_rows, int mode);
+// the sizes the sorted look-ups and the workspace layout belong to and of
+// their payload (never 0).
+uint32_t phase_token(int32_t T, int32_t B, int64_t NS, int32_t E, uint32_t total_rows,
+                     int mode);
 
 // The buffer that holds the sorted look-ups after the sort phase.
 inline uint64_t* sorted_buffer(const BwdLayout& L, char* ws) {

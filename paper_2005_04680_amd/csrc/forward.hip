@@ -11,6 +11,10 @@
 // touched rows would not fit the MALL eight tables at a time walk the bags
 // in dispatch order: all XCDs share the table in progress, and a row read
 // again is served by the MALL instead of HBM.
+//
+// Once a group's offsets are validated its look-up positions are unsigned
+// 32-bit: num_indices may be 2^31 - 1, and the walk reads index windows and
+// load slots past a group's last look-up, which stays below 2^32.
 #include "common.hpp"
 
 namespace embbag {
@@ -126,28 +130,31 @@ __global__ __launch_bounds__(kBlock, MULTI ? (CPL == 1 && MODE == kPoolPlain ? 6
   // the group's last row, and an index outside its table reads row 0: every
   // load is valid, and such slots are masked out of the sum.
   constexpr bool kWin = LPR >= U;
-  int wbase = s0, vcur = 0, vnext = 0;
+  // valid offsets: 0 <= s0 <= s1 <= NS
+  const uint32_t u0 = uint32_t(s0), u1 = uint32_t(s1);
+  uint32_t wbase = u0;
+  int vcur = 0, vnext = 0;
   float acur = 0.f, anext = 0.f;  // per-look-up weights, same windows
   if constexpr (kWin) {
     if (!bad) {
-      vcur = s0 + rl < s1 ? I[s0 + rl] : 0;
-      vnext = s0 + LPR + rl < s1 ? I[s0 + LPR + rl] : 0;
+      vcur = u0 + rl < u1 ? I[u0 + rl] : 0;
+      vnext = u0 + LPR + rl < u1 ? I[u0 + LPR + rl] : 0;
       if constexpr (MODE == kPoolWeighted) {
-        acur = s0 + rl < s1 ? A[s0 + rl] : 0.f;
-        anext = s0 + LPR + rl < s1 ? A[s0 + LPR + rl] : 0.f;
+        acur = u0 + rl < u1 ? A[u0 + rl] : 0.f;
+        anext = u0 + LPR + rl < u1 ? A[u0 + LPR + rl] : 0.f;
       }
     }
   }
 
-  for (int s = s0; s < s1 && !bad; s += U) {
+  for (uint32_t s = u0; s < u1 && !bad; s += U) {
     if constexpr (kWin) {
       if (s - wbase >= LPR) {
         wbase += LPR;
         vcur = vnext;
-        vnext = wbase + LPR + rl < s1 ? I[wbase + LPR + rl] : 0;
+        vnext = wbase + LPR + rl < u1 ? I[wbase + LPR + rl] : 0;
         if constexpr (MODE == kPoolWeighted) {
           acur = anext;
-          anext = wbase + LPR + rl < s1 ? A[wbase + LPR + rl] : 0.f;
+          anext = wbase + LPR + rl < u1 ? A[wbase + LPR + rl] : 0.f;
         }
       }
     }
@@ -156,13 +163,13 @@ __global__ __launch_bounds__(kBlock, MULTI ? (CPL == 1 && MODE == kPoolPlain ? 6
     float wt[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int ss = min(s + u, s1 - 1);
+      const uint32_t ss = min(s + u, u1 - 1);
       int idx;
       if constexpr (kWin) {
         if constexpr (LPR == kWave) {
           // U need not divide LPR: the last slots of an iteration may lie in
           // the next window, which is already loaded (off < LPR + U <= 2 LPR).
-          const int off = ss - wbase;
+          const int off = int(ss - wbase);
           idx = off < LPR ? __builtin_amdgcn_readlane(vcur, off)
                           : __builtin_amdgcn_readlane(vnext, off - LPR);
           if constexpr (MODE == kPoolWeighted)
@@ -171,8 +178,8 @@ __global__ __launch_bounds__(kBlock, MULTI ? (CPL == 1 && MODE == kPoolPlain ? 6
                                        : __builtin_amdgcn_readlane(__float_as_int(anext), off - LPR));
         } else {
           static_assert(LPR % U == 0, "a window must hold whole iterations");
-          idx = __shfl(vcur, rg * LPR + (ss - wbase), kWave);
-          if constexpr (MODE == kPoolWeighted) wt[u] = __shfl(acur, rg * LPR + (ss - wbase), kWave);
+          idx = __shfl(vcur, rg * LPR + int(ss - wbase), kWave);
+          if constexpr (MODE == kPoolWeighted) wt[u] = __shfl(acur, rg * LPR + int(ss - wbase), kWave);
         }
       } else {
         idx = I[ss];
@@ -180,7 +187,7 @@ __global__ __launch_bounds__(kBlock, MULTI ? (CPL == 1 && MODE == kPoolPlain ? 6
       }
       const bool ok = uint32_t(idx) < M;
       if (!ok) err = min(err, EMBBAG_ERR_INDEX_RANGE);
-      use[u] = ok && s + u < s1;
+      use[u] = ok && s + u < u1;
       const uint32_t row = ok ? uint32_t(idx) : 0u;
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
@@ -191,11 +198,11 @@ __global__ __launch_bounds__(kBlock, MULTI ? (CPL == 1 && MODE == kPoolPlain ? 6
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if constexpr (MULTI) {
-        const int ss = s + u;
-        if (ss >= s1 || bad) break;
+        const uint32_t ss = s + u;
+        if (ss >= u1 || bad) break;
         // Crossing the end of bag k (and of any empty bags after it).  While
         // ss < s1 = O[k1] and O is non-decreasing up to s1, k + 1 < k1 here.
-        while (ss >= bound) {
+        while (ss >= uint32_t(bound)) {
           store_bag(k, acc, bound - bstart);
           bstart = bound;
 #pragma unroll

@@ -22,6 +22,9 @@
 // dispatch order, and all XCDs gather from the dY of the table in progress,
 // which the MALL holds.  The W rows, touched once, are read and written with
 // non-temporal hints so they do not evict dY.
+//
+// Sorted positions are unsigned 32-bit: num_indices may be 2^31 - 1, and the
+// walk looks up to two groups past a chunk's end, which stays below 2^32.
 #include <type_traits>
 
 #include "common.hpp"
@@ -163,11 +166,12 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   const int blk = int(logical_block(in_order != 0));
   const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
-  const int lo = chunk * C, hi = min(lo + C, NS);
+  const uint32_t lo = uint32_t(chunk) * uint32_t(C);
+  const uint32_t hi = min(lo + uint32_t(C), uint32_t(NS));
   const double lrd = double(lr);
 
   const uint32_t kprev = lo > 0 ? key_of(sorted[lo - 1]) : kNoKey;
-  const uint32_t knext = hi < NS ? key_of(sorted[hi]) : kNoKey;
+  const uint32_t knext = hi < uint32_t(NS) ? key_of(sorted[hi]) : kNoKey;
   const uint64_t p0 = sorted[lo];
   uint32_t cur = key_of(p0);
   int ct = table_of_bag(bag_of(p0), B, inv_b);
@@ -211,7 +215,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     for (int u = 0; u < U; ++u) an[u] = lo + u < hi ? pd.svals[lo + u] : 0.f;
   }
   uint64_t plast = p0;  // look-up before the current group (none before lo: p0 itself)
-  for (int s = lo; s < hi; s += U) {
+  for (uint32_t s = lo; s < hi; s += U) {
     uint64_t p[U];
     uint32_t bg[U];
     float aw[U];
@@ -384,8 +388,9 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   const int rg = lane / LPR, rl = lane % LPR;
   const int chunk = (int(blockIdx.x) * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
-  const int lo = chunk * C, hi = min(lo + C, NS);
-  if (hi >= NS) return;
+  const uint32_t lo = uint32_t(chunk) * uint32_t(C);
+  const uint32_t hi = min(lo + uint32_t(C), uint32_t(NS));
+  if (hi >= uint32_t(NS)) return;
   // the words around both ends of the chunk, requested together
   const uint64_t wl = sorted[hi - 1], wn = sorted[hi], wf = sorted[lo];
   const uint64_t wb = lo > 0 ? sorted[lo - 1] : ~0ull;

@@ -13,6 +13,9 @@
 // ballots give each lane its rank among equal digits) and written out in
 // digit order, so that the global stores form runs of consecutive addresses.
 // No kernel waits on another workgroup.
+//
+// Look-up positions are unsigned 32-bit: num_indices may be 2^31 - 1, and a
+// tile's last slots run past it (by less than a tile), which stays below 2^32.
 #include "common.hpp"
 
 namespace embbag {
@@ -88,14 +91,14 @@ __global__ __launch_bounds__(kBlock) void build_keys(
   __shared__ uint32_t srowbase[kMaxTables];
   const int tid = threadIdx.x;
   const int blk = blockIdx.x;
-  const int s_lo = blk * TILE;
-  const int s_hi = min(s_lo + TILE, NS);
+  const uint32_t s_lo = uint32_t(blk) * TILE;
+  const uint32_t s_hi = min(s_lo + TILE, uint32_t(NS));
   // The tile's indices are requested first, so that they arrive while the
   // bag search below runs.
   int32_t rv[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const int s = s_lo + i * kBlock + tid;
+    const uint32_t s = s_lo + i * kBlock + tid;
     rv[i] = s < s_hi ? I[s] : 0;
   }
   int err = 0;
@@ -140,7 +143,7 @@ __global__ __launch_bounds__(kBlock) void build_keys(
       // (ceil(log64 TB) dependent loads).  O[lo] <= x holds for valid O; a bad
       // O still leaves the range inside [0, TB - 1].
       const int lane = lane_id();
-      const int x = w == 0 ? s_lo : s_hi - 1;
+      const int x = int(w == 0 ? s_lo : s_hi - 1);
       int lo = 0, hi = TB - 1;
       while (lo < hi) {
         const int step = int((int64_t(hi) - lo + kWave) / kWave);  // ceil((hi - lo + 1) / 64)
@@ -168,14 +171,14 @@ __global__ __launch_bounds__(kBlock) void build_keys(
       for (int q = 0; q < kOq; ++q) {
         const int64_t k = k0 + q * kBlock;
         if (k > k1) break;
-        const int a = max(oa[q], s_lo), b = min(ob[q], s_hi);
-        for (int s = a; s < b; ++s) lbag[s - s_lo] = uint32_t(k);
+        const int a = max(oa[q], int(s_lo)), b = min(ob[q], int(s_hi));
+        for (int s = a; s < b; ++s) lbag[s - int(s_lo)] = uint32_t(k);
       }
     }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
-      const int s = s_lo + i * kBlock + tid;
+      const uint32_t s = s_lo + i * kBlock + tid;
       uint32_t key = 0;
       if (s < s_hi) {
         const uint32_t k = min(lbag[s - s_lo], uint32_t(TB - 1));
@@ -213,18 +216,18 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep(const uint64_t* __restri
   // come in runs (every copy of a hot row is adjacent): within a wavefront,
   // the first lane of each run of equal digits adds the run's length.
   // All of the thread's keys are requested before the first is counted.
-  const int base = blk * (kBlock * IPT);
+  const uint32_t base = uint32_t(blk) * (kBlock * IPT);
   const int lane = lane_id();
   uint32_t kv[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const int s = base + i * kBlock + tid;
-    kv[i] = s < NS ? key_of(src[s]) : 0u;
+    const uint32_t s = base + i * kBlock + tid;
+    kv[i] = s < uint32_t(NS) ? key_of(src[s]) : 0u;
   }
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const int s = base + i * kBlock + tid;
-    const uint32_t dg = s < NS ? (kv[i] >> shift) & (R - 1) : uint32_t(R);
+    const uint32_t s = base + i * kBlock + tid;
+    const uint32_t dg = s < uint32_t(NS) ? (kv[i] >> shift) & (R - 1) : uint32_t(R);
     const uint32_t left = __shfl_up(dg, 1, kWave);
     const bool head = lane == 0 || dg != left;
     const uint64_t heads = __builtin_amdgcn_ballot_w64(head);
@@ -359,14 +362,14 @@ __global__ __launch_bounds__(kBlock, BITS <= 9 ? (VALS ? 3 : 4) : 1) void radix_
   // being key w*64*IPT + i*64 + l: ranking item by item keeps the original
   // order.  The tile is requested first; the digit bases are computed while
   // it is in flight.
-  const int wbase = blk * TILE + w * (kWave * IPT);
+  const uint32_t wbase = uint32_t(blk) * TILE + w * (kWave * IPT);
   uint64_t item[IPT];
   float val[VALS ? IPT : 1];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const int pos = wbase + i * kWave + lane;
-    item[i] = pos < NS ? src[pos] : ~0ull;
-    if constexpr (VALS) val[i] = pos < NS ? vsrc[pos] : 0.f;
+    const uint32_t pos = wbase + i * kWave + lane;
+    item[i] = pos < uint32_t(NS) ? src[pos] : ~0ull;
+    if constexpr (VALS) val[i] = pos < uint32_t(NS) ? vsrc[pos] : 0.f;
   }
 
   // Global start of each digit's run for this tile (thread tid owns digits
@@ -402,7 +405,7 @@ __global__ __launch_bounds__(kBlock, BITS <= 9 ? (VALS ? 3 : 4) : 1) void radix_
   const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const bool valid = wbase + i * kWave + lane < NS;
+    const bool valid = wbase + i * kWave + lane < uint32_t(NS);
     const uint32_t dg = (key_of(item[i]) >> shift) & (R - 1);
     dig[i] = dg;
     uint64_t peers = __builtin_amdgcn_ballot_w64(valid);
@@ -466,7 +469,7 @@ __global__ __launch_bounds__(kBlock, BITS <= 9 ? (VALS ? 3 : 4) : 1) void radix_
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    if (wbase + i * kWave + lane < NS) {
+    if (wbase + i * kWave + lane < uint32_t(NS)) {
       const uint32_t at = whist[w][dig[i]] + rank[i];
       buf[at] = item[i];
       if constexpr (VALS) vbuf[at] = val[i];
@@ -506,8 +509,8 @@ __global__ __launch_bounds__(kBlock) void unique_count(const uint64_t* __restric
   const int tid = threadIdx.x, blk = blockIdx.x;
   uint32_t c = 0;
   for (int i = 0; i < IPT; ++i) {
-    const int s = blk * (kBlock * IPT) + i * kBlock + tid;
-    if (s < NS) {
+    const uint32_t s = uint32_t(blk) * (kBlock * IPT) + i * kBlock + tid;
+    if (s < uint32_t(NS)) {
       const uint64_t p = sorted[s];
       skeys[s] = key_of(p);
       sbags[s] = bag_of(p);
@@ -552,10 +555,10 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
   const int tid = threadIdx.x, blk = blockIdx.x;
   uint32_t running = tile_off[blk];
   for (int i = 0; i < IPT; ++i) {
-    const int s = blk * (kBlock * IPT) + i * kBlock + tid;
+    const uint32_t s = uint32_t(blk) * (kBlock * IPT) + i * kBlock + tid;
     bool head = false;
     uint32_t key = 0;
-    if (s < NS) {
+    if (s < uint32_t(NS)) {
       key = key_of(sorted[s]);
       head = s == 0 || key_of(sorted[s - 1]) != key;
     }
@@ -563,7 +566,7 @@ __global__ __launch_bounds__(kBlock) void unique_write(const uint64_t* __restric
     const uint32_t ex = block_exclusive_scan(head ? 1u : 0u, scratch, &tot);
     if (head) {
       ukeys[running + ex] = key;
-      seg_off[running + ex] = s;
+      seg_off[running + ex] = int32_t(s);
     }
     running += tot;
   }

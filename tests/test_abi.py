@@ -80,7 +80,6 @@ def _tables(rows, dim, ptrs=None):
     ((10,), 8, -1, 1, -1),           # B < 0
     ((10,), 8, 1, -1, -1),           # NS < 0
     ((10,), 8, 1, 2 ** 31, -1),      # NS > INT32_MAX
-    ((10,), 8, 1, 2 ** 31 - 2 ** 16, -1),  # NS above the 2^31 - 1 - 2^16 limit
     ((10,), 8, 0, 5, -4),            # T*B == 0 but NS > 0
 ])
 def test_forward_argument_errors(L, rows, dim, batch, ns, expect):
@@ -126,6 +125,24 @@ def test_workspace_checks(L):
     rows = (C.c_int64 * 2)(10, 10)
     assert L.embbag_dedup(2, rows, 4, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                           dneed - 256, None, None) == -2
+
+
+def test_lookup_limit_is_int32_max(L):
+    """Indices and offsets are int32, so 2^31 - 1 look-ups is the largest
+    count: it passes the argument checks (a workspace of 0 bytes is then
+    refused, before anything is launched) and 2^31 does not.  The oracle draws
+    the line at the same count."""
+    NS = 2 ** 31 - 1
+    assert L.embbag_backward_workspace_bytes(1, 1, NS, 4) >= NS * 16
+    assert L.embbag_backward_workspace_bytes(1, 1, NS + 1, 4) == 0
+    assert L.embbag_dedup_workspace_bytes(1, 1, NS) > 0
+    assert L.embbag_dedup_workspace_bytes(1, 1, NS + 1) == 0
+    t, keep = _tables([10], 8)
+    assert L.embbag_backward_sgd(FAKE, 1, FAKE, FAKE, NS, C.c_float(0.1), C.byref(t), FAKE,
+                                 0, None, None) == -2
+    assert L.embbag_backward_sgd(FAKE, 1, FAKE, FAKE, NS + 1, C.c_float(0.1), C.byref(t), FAKE,
+                                 0, None, None) == -1
+    assert L.embbag_forward(C.byref(t), 1, FAKE, FAKE, NS + 1, FAKE, None, None) == -1
 
 
 def test_large_workspace_is_modest():

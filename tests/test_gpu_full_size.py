@@ -276,15 +276,15 @@ def test_mlperf_split_full_size():
 
 
 def test_maximum_lookup_count():
-    """The most look-ups one call accepts, 2^31 - 1 - 2^16 (the kernels index
-    look-ups in 32 bits and step up to 2^16 past the last one), through the
-    forward and the fused backward: every kernel's index arithmetic at its
-    limit.  One table of 1024 rows, E = 4, bags of 2048 look-ups (the last one
+    """The most look-ups one call accepts, 2^31 - 1 (indices and offsets are
+    int32), through the forward and the fused backward: every kernel's
+    position arithmetic at its limit, where the last radix tile, reduce chunk
+    and index window run past 2^31 - 1.  One table of 1024 rows, E = 4, bags of 2048 look-ups (the last one
     2047) with row s mod 1024, so every full bag reads each row twice.  Weights
     are small integers and gradients binary fractions, so every expected value
     has a closed form that is exact in FP32: each pooled output and every
     updated row must match bit for bit, and no pooled row may stay unwritten."""
-    NS = 2 ** 31 - 1 - 2 ** 16
+    NS = 2 ** 31 - 1
     P, M, E, lr = 2048, 1024, 4, 0.5
     B = (NS + P - 1) // P
     log(f"[full] maximum look-up count: NS={NS}, B={B}, M={M}, E={E}")
@@ -319,17 +319,17 @@ def test_maximum_lookup_count():
 
 
 def test_maximum_lookups_and_bags_together():
-    """Both limits in one call: 2^31 - 1 - 2^16 look-ups and T*B + 1 = 2^31 - 1
-    offsets (2 tables of 2^30 - 1 bags, one look-up per bag, the last 65535
-    bags empty).  This is where the key build's validation slices pass 2^31
-    offsets.  Look-up s of table t reads row (s - t*B) mod 768; B and 768 are
-    multiples of 3, so gradients that depend on the bag index mod 3 give each
-    row a sum with a closed form.  Weights are small integers and gradients
+    """Both limits in one call: 2^31 - 1 look-ups and T*B + 1 = 2^31 - 1
+    offsets (2 tables of 2^30 - 1 bags, one look-up per bag, the last bag
+    two).  This is where the key build's validation slices pass 2^31 offsets.
+    Look-up s of table t reads row (s - t*B) mod 768; B and 768 are multiples
+    of 3, so gradients that depend on the bag index mod 3 give each row a sum
+    with a closed form (the last bag's second look-up is added on its own).  Weights are small integers and gradients
     binary fractions: every pooled output (compared on the device, slice by
     slice) and every updated row must match bit for bit.  About 140 GB of
     device memory."""
     T, B, M, E, lr = 2, 2 ** 30 - 1, 768, 4, 0.5
-    NS, TB = 2 ** 31 - 1 - 2 ** 16, 2 * (2 ** 30 - 1)
+    NS, TB = 2 ** 31 - 1, 2 * (2 ** 30 - 1)
     log(f"[full] maximum look-ups and bags: NS={NS}, T*B+1={TB + 1}, M={M}, E={E}")
     rng = np.random.default_rng(31)
     Wh = rng.integers(-8, 9, (T, M, E)).astype(np.float32)
@@ -337,7 +337,8 @@ def test_maximum_lookups_and_bags_together():
     I = torch.arange(NS, dtype=torch.int32, device=DEV)
     I[B:] -= B
     I.remainder_(M)
-    O = torch.arange(TB + 1, dtype=torch.int32, device=DEV).clamp_(max=NS)
+    O = torch.arange(TB + 1, dtype=torch.int32, device=DEV)
+    O[TB] = NS  # the last bag holds look-ups TB - 1 and TB
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     Y = torch.full((T, B, E), float("nan"), dtype=torch.float32, device=DEV)
     pk.check(pk.embbag_forward(W, B, I, O, Y, status), "forward")
@@ -349,7 +350,7 @@ def test_maximum_lookups_and_bags_together():
         k = torch.arange(lo, min(lo + step, TB), dtype=torch.int64, device=DEV)
         t = torch.div(k, B, rounding_mode="floor")
         exp = Wd[t, (k - t * B) % M]
-        exp[k >= NS] = 0.0
+        exp[k == TB - 1] += Wd[1, B % M]
         got = Yf[lo:lo + k.numel()]
         assert torch.equal(got.view(torch.int32), exp.view(torch.int32)), f"pooled outputs in [{lo}, +{k.numel()})"
     del Y, Yf
@@ -364,11 +365,14 @@ def test_maximum_lookups_and_bags_together():
                      device=DEV)
     pk.check(pk.embbag_backward_sgd(dY, B, I, O, lr, W, ws, status), "backward_sgd")
     pk.check(pk.embbag_status_read(status), "backward status")
-    n = (B, NS - B)  # look-ups of each table
     r = np.arange(M)
     for t in range(T):
-        cnt = np.where(r < n[t], (n[t] - r + M - 1) // M, 0).astype(np.float64)
+        # the first B look-ups of each table: look-up s' in bag t*B + s',
+        # row s' mod M, and bag and row agree mod 3
+        cnt = np.where(r < B, (B - r + M - 1) // M, 0).astype(np.float64)
         G = cnt[:, None] * ((((r % 3) - 1) * 2.0 ** -4)[:, None] + np.arange(E)[None, :] * 2.0 ** -6)
+        if t == T - 1:  # look-up TB (local B) in bag TB - 1: row B mod M
+            G[B % M] += (((TB - 1) % 3) - 1) * 2.0 ** -4 + np.arange(E) * 2.0 ** -6
         Wexp = (Wh[t].astype(np.float64) - lr * G).astype(np.float32)
         assert bits_equal(W[t].cpu().numpy(), Wexp), f"updated rows of table {t}"
     del I, O, dY, dYf, ws

@@ -551,14 +551,49 @@ def test_apply_needs_a_prepared_workspace():
     assert oracle.backward_sgd(G, 100, I, O, 0.1, Wref) == 0
     for t, (a, b) in enumerate(zip(gt.host(), Wref)):
         assert_close(a, b, f"two applies table {t}")
-    # a prepare for other sizes leaves a stamp the apply rejects
-    I2, O2 = random_bags(rng, rows, 100, 10, 0.0, 0.2)
+    # a prepare for other sizes (one look-up more, in the last bag) leaves a
+    # stamp the apply rejects
+    I2 = np.concatenate([I, np.array([3], np.int32)])
+    O2 = O.copy()
+    O2[-1] += 1
     assert pk.embbag_backward_prepare(rows, 32, 100, to_dev(I2), to_dev(O2), ws, gt.status) == 0
     before = gt.host()
-    if I2.size != I.size:
-        assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
-        for a, b in zip(gt.host(), before):
-            assert bits_equal(a, b)
+    assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
+    for a, b in zip(gt.host(), before):
+        assert bits_equal(a, b)
+    assert pk.embbag_status_read(gt.status) == 0
+
+
+def test_apply_rejects_a_prepare_for_another_dim():
+    """The workspace layout depends on E (the carry regions come before the
+    sorted weights), so a weighted prepare for E = 32 applied to E = 64 tables
+    must write nothing; prepared for E = 64 the same apply is the oracle's."""
+    import paper_2005_04680_amd as pk
+    rng = np.random.default_rng(23)
+    rows, batch = (300, 200), 50
+    W = _tables(rng, rows, 64, 0.05)
+    I, O = random_bags(rng, rows, batch, 12, 0.1, 0.3)
+    G = rng.standard_normal((2, batch, 64)).astype(np.float32)
+    a = rng.uniform(-2, 2, I.size).astype(np.float32)
+    gt = GpuTables(W)
+    Id, Od, Gd, ad = to_dev(I), to_dev(O), to_dev(G), to_dev(a)
+    nbytes = max(pk.embbag_backward_workspace_bytes(2, batch, I.size, e) for e in (32, 64))
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device=DEV)
+    assert pk.embbag_backward_prepare_pooled(rows, 32, batch, Id, Od, ws, ad,
+                                             pk.EMBBAG_POOL_SUM, gt.status) == 0
+    assert pk.embbag_backward_apply_sgd_pooled(Gd, batch, Od, I.size, 0.1, gt.w, ws, ad,
+                                               pk.EMBBAG_POOL_SUM) == 0
+    for x, y in zip(gt.host(), W):
+        assert bits_equal(x, y)
+    assert pk.embbag_backward_prepare_pooled(rows, 64, batch, Id, Od, ws, ad,
+                                             pk.EMBBAG_POOL_SUM, gt.status) == 0
+    assert pk.embbag_backward_apply_sgd_pooled(Gd, batch, Od, I.size, 0.1, gt.w, ws, ad,
+                                               pk.EMBBAG_POOL_SUM) == 0
+    assert pk.embbag_status_read(gt.status) == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd_weighted(G, batch, I, O, 0.1, Wref, a, oracle.POOL_SUM) == 0
+    for t, (x, y) in enumerate(zip(gt.host(), Wref)):
+        assert_close(x, y, f"weighted apply table {t}")
 
 
 # ---------------------------------------------------------------------------
