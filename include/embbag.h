@@ -116,6 +116,26 @@ int embbag_backward_sgd(const float* grad_pooled, int32_t batch, const int32_t* 
                         const embbag_tables_t* tables, void* workspace, size_t workspace_bytes,
                         int32_t* d_status, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation as embbag_backward_sgd, with the same arguments but no workspace,
+ * and the same kernels.  Its workspace is a fixed device array of
+ * EMBBAG_NOALLOC_SCRATCH_BYTES (64 MiB) inside the library, which each GPU it
+ * runs on holds from its first call until the process ends; the call itself
+ * allocates nothing.  A step whose workspace (embbag_backward_workspace_bytes)
+ * exceeds the array is refused with EMBBAG_ERR_WORKSPACE and enqueues nothing
+ * (64 MiB holds 8 tables x 2048 bags x 32 look-ups at E = 64, 30.5 MiB, or
+ * 819,200 look-ups at E = 64, 47.7 MiB).  Argument errors are those of
+ * embbag_backward_sgd.  Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (other streams, other threads) race; calls ordered
+ * on one stream are safe.  EMBBAG_ERR_HIP if the array's device address
+ * cannot be obtained. */
+#define EMBBAG_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int embbag_backward_sgd_noalloc(const float* grad_pooled, int32_t batch, const int32_t* indices,
+                                const int32_t* offsets, int64_t num_indices, float lr,
+                                const embbag_tables_t* tables, int32_t* d_status,
+                                hipStream_t stream);
+
 /* Pooling modes of the *_pooled entry points (Section II: L = A^T W, where
  * column n of A holds a weight a_p for every row bag n reads). */
 #define EMBBAG_POOL_SUM 0  /* Y[k] = sum over s of a_s * W[I[s]] (a_s = 1 without weights) */

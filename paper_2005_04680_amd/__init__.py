@@ -28,6 +28,7 @@ EMBBAG_ERR_OFFSETS = -4
 EMBBAG_ERR_HIP = -5
 EMBBAG_POOL_SUM = 0
 EMBBAG_POOL_MEAN = 1
+EMBBAG_NOALLOC_SCRATCH_BYTES = 64 << 20  # the no-allocation entry point's fixed workspace
 
 
 class EmbbagError(RuntimeError):
@@ -92,6 +93,7 @@ def lib():
         L.embbag_baseline_update_owner.argtypes = [p, i32, p, p, i64, C.c_float, p, i32, p]
         L.embbag_baseline_touch_rows.argtypes = [i32, i64, p, p, sz, p]
         L.embbag_status_read.argtypes = [p, p]
+        L.embbag_backward_sgd_noalloc.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
                   "embbag_backward_sgd_split_bf16", "embbag_backward_prepare",
                   "embbag_forward_pooled", "embbag_backward_sgd_pooled",
@@ -102,7 +104,8 @@ def lib():
                   "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
                   "embbag_baseline_materialize", "embbag_baseline_update_atomic",
                   "embbag_baseline_backward_sgd_atomic", "embbag_baseline_update_owner",
-                  "embbag_baseline_touch_rows", "embbag_status_read"):
+                  "embbag_baseline_touch_rows", "embbag_status_read",
+                  "embbag_backward_sgd_noalloc"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -329,6 +332,19 @@ def embbag_backward_sgd(grad_pooled, batch, indices, offsets, lr, weights, works
                                      float(lr), C.byref(s), _ptr(workspace, None, "workspace"),
                                      int(workspace.numel() * workspace.element_size()),
                                      _status_ptr(d_status), _stream(stream))
+
+
+def embbag_backward_sgd_noalloc(grad_pooled, batch, indices, offsets, lr, weights,
+                                d_status=None, stream=None) -> int:
+    """embbag_backward_sgd with the library's fixed device scratch array as its
+    workspace (no allocation; EMBBAG_ERR_WORKSPACE past its size)."""
+    _check_bags(len(weights), batch, offsets)
+    _check_act(grad_pooled, len(weights), batch, _check_tables(weights), "grad_pooled")
+    s, keep = _tables_struct(weights)
+    return lib().embbag_backward_sgd_noalloc(
+        _ptr(grad_pooled, _dt("float32"), "grad_pooled"), int(batch),
+        _ptr(indices, _dt(*_I32), "indices"), _ptr(offsets, _dt(*_I32), "offsets"),
+        int(indices.numel()), float(lr), C.byref(s), _status_ptr(d_status), _stream(stream))
 
 
 def embbag_backward_sgd_split_bf16(grad_pooled, batch, indices, offsets, lr, hi, lo, workspace,

@@ -140,6 +140,18 @@ int main() {
          "backward: batch < 0");
   expect(embbag_backward_sgd_pooled(G, 8, I, O, 64, nullptr, 9, 0.1f, &tb, ws, wsb, stt, st),
          kInv, "backward: pooling mode");
+  // the no-allocation backward reports argument errors before it looks up
+  // its scratch array, and refuses a step larger than the array
+  expect(embbag_backward_sgd_noalloc(G, 8, I, O, 64, 0.1f, nullptr, stt, st), kInv,
+         "no-allocation backward: no tables");
+  expect(embbag_backward_sgd_noalloc(nullptr, 8, I, O, 64, 0.1f, &tb, stt, st), kInv,
+         "no-allocation backward: no gradient");
+  expect(embbag_backward_sgd_noalloc(G, 8, I, O, int64_t(2147483648), 0.1f, &tb, stt, st), kInv,
+         "no-allocation backward: NS over the limit");
+  expect(embbag_backward_sgd_noalloc(G, 8, I, nullptr, 64, 0.1f, &tb, stt, st), kInv,
+         "no-allocation backward: no offsets");
+  expect(embbag_backward_sgd_noalloc(G, 8, I, O, int64_t(1) << 30, 0.1f, &tb, stt, st), kWs,
+         "no-allocation backward: step past the scratch array");
   expect(embbag_backward_prepare(0, rows, 16, 8, I, O, 64, ws, wsb, stt, st), kInv,
          "prepare: table count");
   expect(embbag_backward_prepare(3, rows, 16, 8, I, nullptr, 64, ws, wsb, stt, st), kInv,
