@@ -81,18 +81,16 @@ def bytes_model(cfg, U, split, act_bf16=False, weighted=False):
 
 
 def profiled_traffic(workload, call):
-    """HBM-side bytes per launch of one call ("forward" or "apply", all its
-    kernels) from profiles/traffic.json (copy-calibrated rocprofv3 FETCH_SIZE +
-    WRITE_SIZE), or None when that record is for another workload or the
-    kernels' sources changed since the counters were taken."""
+    """L2-to-fabric bytes per launch of one call ("forward", "prepare" or
+    "apply", all its kernels) from profiles/traffic.json (copy-calibrated
+    rocprofv3 FETCH_SIZE + WRITE_SIZE), or None when the record holds no such
+    workload or the kernels' sources changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("workload") != workload:
-        return None
-    r = rec.get("calls", {}).get(call)
+    r = rec.get("workloads", {}).get(workload, {}).get("calls", {}).get(call)
     if r is None:
         return None
     h = hashlib.sha256()
@@ -139,10 +137,39 @@ def host_ram_gb():
     return None
 
 
-def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
+def host_tables(pk, torch, cfg):
+    """Every table of the workload in host memory, filled from the counter-based
+    generator on the device (for split storage: the hi and lo halves)."""
+    from embbag_data import fill_table_torch
+    out, out_lo = [], []
+    for t, m in enumerate(cfg.rows):
+        tmp = torch.empty((m, cfg.dim), dtype=torch.float32, device="cuda")
+        fill_table_torch(cfg, t, tmp)
+        if cfg.split:
+            hi = torch.empty((m, cfg.dim), dtype=torch.int16, device="cuda")
+            lo = torch.empty((m, cfg.dim), dtype=torch.int16, device="cuda")
+            pk.check(pk.embbag_split_fp32(tmp, hi, lo), "split")
+            del tmp
+            out.append(hi.cpu().numpy().view(np.uint16))
+            out_lo.append(lo.cpu().numpy().view(np.uint16))
+            del hi, lo
+        else:
+            out.append(tmp.cpu().numpy())
+            del tmp
+    torch.cuda.synchronize()
+    return out, out_lo
+
+
+def cpu_baseline(pk, cfg, host_batches, sample_bags, act_bf16=False, pooling="sum",
+                 budget_s=25.0):
     """The CPU oracle on the first `sample_bags` bags of every table of each of
     `host_batches` ((indices, grads, weights or None) on the host), forward +
-    fused backward."""
+    fused backward, single-threaded on one host core, stopping after the batch
+    that takes it past `budget_s`.  Full-table mode (whole tables in host
+    memory, the look-ups reading them at random as on the GPU) where host RAM
+    holds 1.1x the tables; otherwise touched-rows mode (each table compacted to
+    the rows the sample touches, regenerated from the counter-based generator:
+    less memory, and more locality than the full tables would give)."""
     import torch
 
     import oracle
@@ -150,27 +177,44 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
 
     P, B, T = cfg.pooling, cfg.batch, cfg.num_tables
     nb = min(sample_bags, B)
-    dt, dt_f, dt_b, n_look, n_rows = 0.0, 0.0, 0.0, 0, 0
+    ram = host_ram_gb()
+    full = ram is not None and ram * 1e9 >= 1.1 * cfg.table_bytes
+    mode = "full-table" if full else "touched-rows"
+    t_fill = time.perf_counter()
+    if full:
+        full_w, full_lo = host_tables(pk, torch, cfg)
+    t_fill = time.perf_counter() - t_fill
+    dt, dt_f, dt_b, n_look, n_rows, n_batches = 0.0, 0.0, 0.0, 0, 0, 0
     # one host core for the whole timed region (the oracle is single-threaded)
     old_aff = os.sched_getaffinity(0)
     core = min(old_aff)
     os.sched_setaffinity(0, {core})
     for batch_I, G, A in host_batches:
+        if dt > budget_s:
+            break
         I_s, tabs, A_s = [], [], []
         for t in range(T):
             part = batch_I[t * B * P: t * B * P + nb * P]
+            if A is not None:
+                A_s.append(A[t * B * P: t * B * P + nb * P])
+            if full:
+                I_s.append(part)
+                n_rows += np.unique(part).size
+                continue
             rows, inv = np.unique(part, return_inverse=True)
             n_rows += rows.size
             I_s.append(inv.astype(np.int32))
-            if A is not None:
-                A_s.append(A[t * B * P: t * B * P + nb * P])
             vals = table_rows_torch(cfg.seed, t, torch.from_numpy(rows).cuda(), cfg.dim,
                                     cfg.value_scale[t])
             tabs.append(vals.cpu().numpy())
+        if full:
+            tabs = full_w
         I_s = np.concatenate(I_s)
         O_s = np.arange(0, T * nb * P + 1, P, dtype=np.int32)
         G_s = np.ascontiguousarray(G[:, :nb, :])
-        if cfg.split:
+        if cfg.split and full:
+            his, los = full_w, full_lo
+        elif cfg.split:
             his, los = zip(*[oracle.split(w) for w in tabs])
             his, los = list(his), list(los)
             del tabs
@@ -200,14 +244,87 @@ def cpu_baseline(cfg, host_batches, sample_bags, act_bf16=False, pooling="sum"):
         dt += t2 - t0
         assert rc1 == 0 and rc2 == 0
         n_look += I_s.size
+        n_batches += 1
     os.sched_setaffinity(0, old_aff)
+    if full:
+        del full_w, full_lo
+    where = (f"the whole tables in host memory ({cfg.table_bytes / 1e9:.1f} GB, filled in "
+             f"{t_fill:.0f} s, not timed)" if full else
+             f"tables compacted to the sampled look-ups' rows (host RAM {ram} GB < 1.1x "
+             f"{cfg.table_bytes / 1e9:.1f} GB of tables)")
     return {"value": n_look / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "sample": (f"first {nb} of {B} bags of each of the {T} tables of batches "
-                       f"0-{len(host_batches) - 1} ({n_look} look-ups, {n_rows} touched rows), "
-                       f"forward + fused backward/SGD, single-threaded, {dt:.2f} s"),
+            "mode": mode,
+            "sample": (f"{mode}: first {nb} of {B} bags of each of the {T} tables of batches "
+                       f"0-{n_batches - 1} ({n_look} look-ups, {n_rows} touched rows) on "
+                       f"{where}, forward + fused backward/SGD, single-threaded, {dt:.2f} s"),
             "host": host_cpu(), "core": core,
             "forward_lookups_per_s": round(n_look / dt_f, 1),
             "backward_sgd_lookups_per_s": round(n_look / dt_b, 1)}
+
+
+def calibrate_gather(pk, torch, dev, reps=10):
+    """Measured rates of the access patterns the step is made of, on this GPU:
+    random whole-row reads (each row once; the library's forward with one
+    look-up per bag, which reads the rows and writes them out densely, and
+    torch.index_select as a library reference), the same rows in increasing
+    order, and random whole-row read-modify-writes (the update's floor kernel,
+    each row read and written back once), for 1 KB rows (E = 256) and 512 B rows
+    (E = 128), 3.3M distinct rows of a 6.1 GB table.  Also random 512 B reads of
+    every row of an 872 MB array (the MLPerf-shaped gradient, read once in a
+    random order by the update)."""
+    def timed(fn):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(20050468)
+    out = {"calibration": "gather", "reps": reps}
+    U = 3276528
+    for E, M in ((256, 6_000_000), (128, 12_000_000)):
+        row = 4 * E
+        w = torch.empty((M, E), dtype=torch.float32, device=dev)
+        w.normal_(generator=g)
+        rows = torch.randperm(M, generator=g, device=dev)[:U].to(torch.int32)
+        srt = torch.sort(rows).values
+        O = torch.arange(U + 1, dtype=torch.int32, device=dev)
+        Y = torch.empty((1, U, E), dtype=torch.float32, device=dev)
+        status = torch.zeros(1, dtype=torch.int32, device=dev)
+        r = {"row_bytes": row, "rows": U, "table_gb": round(M * row / 1e9, 2)}
+        for name, idx in (("random", rows), ("sorted", srt)):
+            ms = timed(lambda: pk.check(pk.embbag_forward([w], U, idx, O, Y, status), "forward"))
+            r[f"read_{name}_ms"] = round(ms, 4)
+            r[f"read_{name}_gbps"] = round(U * row / (ms * 1e-3) / 1e9, 1)
+            r[f"read_{name}_plus_write_gbps"] = round(2 * U * row / (ms * 1e-3) / 1e9, 1)
+        il = rows.to(torch.int64)
+        ms = timed(lambda: torch.index_select(w, 0, il))
+        r["index_select_random_plus_write_gbps"] = round(2 * U * row / (ms * 1e-3) / 1e9, 1)
+        ws = torch.empty(pk.embbag_backward_workspace_bytes(1, U, U, E), dtype=torch.uint8,
+                         device=dev)
+        pk.check(pk.embbag_backward_prepare([M], E, U, rows, O, ws, status), "prepare")
+        ms = timed(lambda: pk.check(pk.embbag_baseline_touch_rows(U, U, [w], ws), "touch"))
+        r["rmw_random_ms"] = round(ms, 4)
+        r["rmw_random_gbps"] = round(2 * U * row / (ms * 1e-3) / 1e9, 1)
+        assert pk.embbag_status_read(status) == 0
+        out[f"rows_{row}B"] = r
+        del w, rows, srt, O, Y, ws, il
+        torch.cuda.empty_cache()
+    n, E = 65536 * 26, 128
+    a = torch.empty((n, E), dtype=torch.float32, device=dev)
+    a.normal_(generator=g)
+    perm = torch.randperm(n, generator=g, device=dev)
+    ms = timed(lambda: torch.index_select(a, 0, perm))
+    out["perm_read_512B"] = {"array_mb": round(n * E * 4 / 1e6, 1),
+                             "ms": round(ms, 4),
+                             "read_gbps": round(n * E * 4 / (ms * 1e-3) / 1e9, 1),
+                             "read_plus_write_gbps": round(2 * n * E * 4 / (ms * 1e-3) / 1e9, 1)}
+    return out
 
 
 def time_graph(torch, batches, prep, fwd, apply, K, warmup):
@@ -301,6 +418,9 @@ def main():
                     help="pooled outputs and their gradients in FP32, or in BF16 (split-storage "
                          "configurations only: Section VII's BF16 activations)")
     ap.add_argument("--batches", type=int, default=8, help="pre-generated batches, rotated")
+    ap.add_argument("--table-alloc", default="separate", choices=["separate", "one"],
+                    help="FP32 tables as one device allocation each, or as row ranges of a "
+                         "single allocation")
     ap.add_argument("--cpu-sample-bags", type=int, default=8192,
                     help="bags per table of each sampled batch the CPU oracle is timed on")
     ap.add_argument("--cpu-sample-batches", type=int, default=3,
@@ -316,6 +436,9 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="also time the step captured as one HIP graph per batch and replayed "
                          "(for the launch-bound small workloads)")
+    ap.add_argument("--calibrate-gather", action="store_true",
+                    help="only measure random row reads and read-modify-writes of 1 KB and "
+                         "512 B rows (the access patterns of the step) on this GPU")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE to bytes)")
@@ -339,6 +462,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calibrate_gather:
+        print(json.dumps(calibrate_gather(pk, torch, dev)), flush=True)
+        return
     if args.calibrate_copy:
         n = 1 << 28  # 1 GiB of FP32
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -381,6 +507,11 @@ def main():
             pk.check(pk.embbag_split_fp32(tmp, hi[t], lo[t]), "split")
             del tmp
         tables = None
+    elif args.table_alloc == "one":
+        whole = torch.empty((sum(cfg.rows), E), dtype=torch.float32, device=dev)
+        base = np.concatenate([[0], np.cumsum(cfg.rows)])
+        tables = [whole[int(base[t]):int(base[t + 1])] for t in range(T)]
+        fill_tables_torch(cfg, tables)
     else:
         tables = [torch.empty((m, E), dtype=torch.float32, device=dev) for m in cfg.rows]
         fill_tables_torch(cfg, tables)
@@ -522,11 +653,23 @@ def main():
     else:
         roof_call, roof_k, roof_b, roof_ms = "forward", "fwd_gather_sum", fwd_b, fwd_ms
     achieved = roof_b / (roof_ms * 1e-3) / 1e9
+    wtag = workload_tag(cfg, act_bf16, args.pooling)
     roof = {"kernel": roof_k, "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": profiled_traffic(workload_tag(cfg, act_bf16, args.pooling), roof_call),
+            "traffic": profiled_traffic(wtag, roof_call),
             "bytes_per_launch": int(roof_b),
             "avg_launch_ms": round(roof_ms, 4)}
+    # Measured bytes of the whole step: the counter traffic (L2-to-fabric
+    # fetch + write, which MALL hits also count) of the forward, prepare and
+    # apply calls, per step, over the step time.
+    calls = [profiled_traffic(wtag, c) for c in ("forward", "prepare", "apply")]
+    step_traffic = None
+    if all(c is not None for c in calls):
+        tb = sum(calls)
+        step_traffic = {"bytes": int(tb), "gbps": round(tb / (ms_step * 1e-3) / 1e9, 1),
+                        "pct_hbm_peak": round(100 * tb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+                        "forward_bytes": int(calls[0]), "prepare_bytes": int(calls[1]),
+                        "apply_bytes": int(calls[2])}
     if roof_call == "apply" and not split and not pooled:
         # The apply's floor on this GPU: the read and write-back of the same
         # touched rows with nothing summed (no gradient gathers).
@@ -553,14 +696,20 @@ def main():
                    "batch": B,
                    "pooling": cfg.pooling, "num_indices": NS, "unique_rows": round(U_avg),
                    "lr": cfg.lr, "batches_rotated": args.batches,
+                   "table_alloc": args.table_alloc,
                    "streams": 2 if args.overlap_prepare else 1},
         "ms_per_step_median": round(float(np.median(per_step)), 4),
         "ms_per_step_p90": round(float(np.percentile(per_step, 90)), 4),
         "gbps_alg": round(gbps, 1),
         "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+        "pct_hbm_peak_model": ("algorithmic bytes, every look-up's whole row read counted as "
+                               "Section II frames it (GUPS-like); on Zipf data repeated rows are "
+                               "L2/MALL hits, so this exceeds the HBM-delivered share"),
         "bytes_alg_per_step": int(step_b),
         "gbps_min": round(gbps_min, 1),
+        "pct_hbm_peak_min": round(100 * gbps_min / HBM_PEAK_GBPS, 2),
         "bytes_min_per_step": int(step_min_b),
+        "traffic_step": step_traffic,
         "fwd_ms": round(fwd_ms, 4),
         "bwd_prepare_ms": round(prep_ms, 4),
         "bwd_apply_ms": round(apply_ms, 4),
@@ -576,7 +725,7 @@ def main():
     if not args.no_cpu_baseline:
         host = [(bt["I_host"], bt["G_host"], bt["A_host"]) for bt in batches
                 if bt["I_host"] is not None]
-        out["cpu_baseline"] = cpu_baseline(cfg, host, args.cpu_sample_bags, act_bf16,
+        out["cpu_baseline"] = cpu_baseline(pk, cfg, host, args.cpu_sample_bags, act_bf16,
                                            args.pooling)
     print(json.dumps(out), flush=True)
 

@@ -281,7 +281,7 @@ def test_split_bf16_activation_argument_errors():
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("case", ["tiny", "random", "p1_hot", "small", "mlperf_scaled",
                                   "tile1024", "tile2048", "tile4096", "one_pass", "digits7",
-                                  "four_passes"])
+                                  "four_passes", "hot_17bit", "hot_24bit", "hot_2m"])
 def test_dedup_bit_exact(case):
     rng = np.random.default_rng(5)
     if case == "tiny":
@@ -302,6 +302,14 @@ def test_dedup_bit_exact(case):
         cfg = scaled(get_config("mlperf"), batch=8192)
         rows, batch = cfg.rows, cfg.batch
         I, O = make_batch(cfg, 0)
+    elif case.startswith("hot_"):
+        # row 0 of each table takes half or more of its look-ups (runs of equal
+        # digits spanning many radix tiles in every pass): 17-bit keys (two
+        # passes), 24-bit keys (three passes), and 21-bit keys over 2M look-ups
+        rows, batch, pool, hot = {"hot_17bit": ((100000, 31072), 3000, 20, 0.5),
+                                  "hot_24bit": ((8000000, 8777215), 3000, 20, 0.5),
+                                  "hot_2m": ((2 ** 20, 2 ** 20), 16000, 130, 0.6)}[case]
+        I, O = random_bags(rng, rows, batch, pool, 0.05, hot)
     elif case in ("one_pass", "digits7", "four_passes"):
         # key widths the other cases miss (the dedup needs row counts only, no
         # tables): 9-bit keys sorted in one pass, 21-bit keys in three passes of
