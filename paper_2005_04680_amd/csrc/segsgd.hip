@@ -8,10 +8,14 @@
 // it to an FP64 accumulator; when the key changes, the finished segment is
 //   * applied, W[row] <- W[row] - lr * G, if it began and ended inside the
 //     chunk (the W row was requested with the look-up that began it), or
-//   * parked as a partial sum in the carry buffer: slot 2c for the chunk's
-//     first segment, slot 2c+1 for its last one.
-// A second kernel gives every segment that crosses chunk boundaries to the
-// chunk where it begins; that chunk adds its own partial and the partials
+//   * with 64-lane rows, applied as well if it began in the chunk and ends
+//     within the next chunk's first 64 look-ups: the wavefront walks on to
+//     its end, and the next chunk starts its walk after it, so short segments
+//     need no carry;
+//   * otherwise parked as a partial sum in the carry buffer: slot 2c for the
+//     chunk's first segment, slot 2c+1 for its last one.
+// A second kernel gives every other segment that crosses a chunk boundary to
+// the chunk where it begins; that chunk adds its own partial and the partials
 // of the following chunks, in chunk order, and applies the row once.  Every
 // touched row is therefore read and written exactly once, with a sum order
 // that does not depend on scheduling (the result is bit-reproducible).
@@ -24,7 +28,8 @@
 // non-temporal hints so they do not evict dY.
 //
 // Sorted positions are unsigned 32-bit: num_indices may be 2^31 - 1, and the
-// walk looks up to two groups past a chunk's end, which stays below 2^32.
+// walks look at most 64 look-ups and two groups past a chunk's end, which
+// stays below 2^32.
 #include <type_traits>
 
 #include "common.hpp"
@@ -141,6 +146,14 @@ struct PoolDev {
 };
 
 
+// Lane i's copy of a 64-bit word held one per lane (i the same across the
+// wavefront).
+__device__ __forceinline__ uint64_t word_of_lane(uint64_t w, int i) {
+  const uint32_t l = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(w)), i));
+  const uint32_t h = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(w >> 32)), i));
+  return (uint64_t(h) << 32) | l;
+}
+
 template <int LPR, int CPL, class Rows, int MODE, bool GBF16>
 __global__ __launch_bounds__(kBlock) void segment_sgd(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
@@ -167,16 +180,89 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
   const int chunk = (blk * kWavesPerBlock + wave_id()) * R + rg;
   if (chunk >= nchunks) return;
   const uint32_t lo = uint32_t(chunk) * uint32_t(C);
-  const uint32_t hi = min(lo + uint32_t(C), uint32_t(NS));
+  const uint32_t hi0 = min(lo + uint32_t(C), uint32_t(NS));
   const double lrd = double(lr);
+  constexpr bool kW = MODE == kPoolWeighted;
+  // With 64 lanes per row (one row group per wavefront), a segment that
+  // crosses into the next chunk and ends within its first 64 look-ups is
+  // walked to its end here; with several row groups per wavefront the longer
+  // walk would hold up the others, and every crossing segment is carried.
+  constexpr bool kWin = LPR == kWave;
 
   const uint32_t kprev = lo > 0 ? key_of(sorted[lo - 1]) : kNoKey;
-  const uint32_t knext = hi < uint32_t(NS) ? key_of(sorted[hi]) : kNoKey;
-  const uint64_t p0 = sorted[lo];
+  const uint32_t knext0 = hi0 < uint32_t(NS) ? key_of(sorted[hi0]) : kNoKey;
+  uint32_t hi = hi0, knext = knext0;  // end of the walk, key just past it
+  uint32_t s0 = lo;                   // start of the walk
+  bool first_open;                    // first segment walked began before s0
+  bool is_first = true;
+  // Software pipeline: the (key, bag) words of the next U look-ups are loaded
+  // while the current ones are summed; for the current U look-ups, the dY rows
+  // (skipped when a look-up repeats the previous (key, bag) pair: its row is
+  // still in registers) and the W rows of the segments that start among them
+  // are all requested before the first of them is used.
+  // Weighted bags: each look-up's weight is loaded one group ahead, with its
+  // word (the weights were sorted along with the look-ups).
+  uint64_t pn[U];
+  float an[U];
+  if constexpr (kWin) {
+    // Requested with the keys above: the key before the previous chunk, the
+    // words of the chunk's first 64 look-ups and the keys of the 64 past its
+    // end, one per lane.
+    const uint32_t klast = key_of(sorted[hi0 - 1]);
+    const uint32_t kpp = lo > uint32_t(C) ? key_of(sorted[lo - uint32_t(C) - 1]) : kNoKey;
+    const uint64_t wlead = lo + lane < hi0 ? sorted[lo + lane] : ~0ull;
+    const float alead = kW && lo + lane < hi0 ? pd.svals[lo + lane] : 0.f;
+    const uint32_t kpast = hi0 + lane < uint32_t(NS) ? key_of(sorted[hi0 + lane]) : kNoKey;
+    // The last segment began in this chunk, continues in the next and ends
+    // within its first 64 look-ups: the walk goes on to its end, and the
+    // segment is applied here.
+    if (knext0 == klast && kprev != klast) {
+      const uint64_t m = __builtin_amdgcn_ballot_w64(kpast != klast);
+      if (m != 0ull) {
+        const int e = int(__builtin_ctzll(m));
+        hi = hi0 + uint32_t(e);
+        knext = uint32_t(__builtin_amdgcn_readlane(int(kpast), e));
+      }
+    }
+    // The first segment began in the previous chunk and ends within this
+    // chunk's first 64 look-ups: the previous chunk applied it, and the walk
+    // starts after it.
+    first_open = kprev == key_of(word_of_lane(wlead, 0));
+    if (first_open && kpp != kprev) {
+      const uint64_t m = __builtin_amdgcn_ballot_w64(key_of(wlead) != kprev);
+      if (m != 0ull) {
+        s0 = lo + uint32_t(__builtin_ctzll(m));
+        if (s0 >= hi0) return;  // the whole chunk was that segment
+        first_open = false;
+        is_first = false;  // a segment left open at the end takes slot 2c+1
+      }
+    }
+    // the first U words from the lanes that hold them
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t q = s0 + uint32_t(u);
+      const int i = int(q - lo);
+      if (i < kWave) {
+        pn[u] = q < hi ? word_of_lane(wlead, i) : 0ull;
+        if constexpr (kW)
+          an[u] = q < hi ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alead), i)) : 0.f;
+      } else {
+        pn[u] = q < hi ? sorted[q] : 0ull;
+        if constexpr (kW) an[u] = q < hi ? pd.svals[q] : 0.f;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < U; ++u) pn[u] = lo + u < hi0 ? sorted[lo + u] : 0ull;
+    if constexpr (kW) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) an[u] = lo + u < hi0 ? pd.svals[lo + u] : 0.f;
+    }
+    first_open = kprev == key_of(pn[0]);
+  }
+  const uint64_t p0 = pn[0];
   uint32_t cur = key_of(p0);
   int ct = table_of_bag(bag_of(p0), B, inv_b);
-  const bool first_open = kprev == cur;  // first segment began in an earlier chunk
-  bool is_first = true;
 
   d4 acc[CPL];
   f4 glast[CPL];
@@ -198,24 +284,8 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
     }
   };
 
-  // Software pipeline: the (key, bag) words of the next U look-ups are loaded
-  // while the current ones are summed; for the current U look-ups, the dY rows
-  // (skipped when a look-up repeats the previous (key, bag) pair: its row is
-  // still in registers) and the W rows of the segments that start among them
-  // are all requested before the first of them is used.
-  // Weighted bags: each look-up's weight is loaded one group ahead, with its
-  // word (the weights were sorted along with the look-ups).
-  constexpr bool kW = MODE == kPoolWeighted;
-  uint64_t pn[U];
-  float an[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) pn[u] = lo + u < hi ? sorted[lo + u] : 0ull;
-  if constexpr (kW) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) an[u] = lo + u < hi ? pd.svals[lo + u] : 0.f;
-  }
-  uint64_t plast = p0;  // look-up before the current group (none before lo: p0 itself)
-  for (uint32_t s = lo; s < hi; s += U) {
+  uint64_t plast = p0;  // look-up before the current group (none before s0: p0 itself)
+  for (uint32_t s = s0; s < hi; s += U) {
     uint64_t p[U];
     uint32_t bg[U];
     float aw[U];
@@ -234,7 +304,7 @@ __global__ __launch_bounds__(kBlock) void segment_sgd(
       const uint64_t pq = u == 0 ? plast : p[u - 1];
       const bool valid = s + u < hi;
       // a repeat of the previous look-up's (key, bag): its dY row is reused
-      dup[u] = valid && p[u] == pq && !(s == lo && u == 0);
+      dup[u] = valid && p[u] == pq && !(s == s0 && u == 0);
       nseg[u] = valid && key_of(p[u]) != key_of(pq);
     }
     if constexpr (MODE == kPoolMean) {
@@ -365,9 +435,14 @@ __global__ __launch_bounds__(kBlock) void carry_group(
   }
 }
 
-// Segments that cross chunk boundaries: the chunk where one begins sums the
-// partials in chunk order (a filled group's pre-summed value in place of its
-// chunks) and applies the row.
+// Segments carried across chunk boundaries: the chunk where one begins sums
+// the partials in chunk order (a filled group's pre-summed value in place of
+// its chunks) and applies the row.  With 64 lanes per row a wavefront takes a
+// group of kCarryGroup chunks, finds which of them start such a segment (all
+// boundary words requested at once, one chunk per lane) and fixes those up
+// one after another: with short segments applied by the update, most groups
+// hold none and few hold more than two.  Narrower rows take one chunk per
+// row group.
 template <int LPR, int CPL, class Rows, int MODE>
 __global__ __launch_bounds__(kBlock) void segment_fixup(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
@@ -386,122 +461,154 @@ __global__ __launch_bounds__(kBlock) void segment_fixup(
   const int E = d.dim, E4 = E / 4;
   const int lane = lane_id();
   const int rg = lane / LPR, rl = lane % LPR;
-  const int chunk = (int(blockIdx.x) * kWavesPerBlock + wave_id()) * R + rg;
-  if (chunk >= nchunks) return;
-  const uint32_t lo = uint32_t(chunk) * uint32_t(C);
-  const uint32_t hi = min(lo + uint32_t(C), uint32_t(NS));
-  if (hi >= uint32_t(NS)) return;
-  // the words around both ends of the chunk, requested together
-  const uint64_t wl = sorted[hi - 1], wn = sorted[hi], wf = sorted[lo];
-  const uint64_t wb = lo > 0 ? sorted[lo - 1] : ~0ull;
-  const uint32_t kl = key_of(wl);
-  if (key_of(wn) != kl) return;             // last segment ends here
-  const uint32_t kf = key_of(wf);
-  if (kf == kl && lo > 0 && key_of(wb) == kl) return;  // began earlier
-  const int ct = table_of_bag(bag_of(wl), B, inv_b);
-  const uint32_t r = kl - tb.rowbase[ct];
-  const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
-
-  d4 acc[CPL];
-  typename Rows::Pre pre[CPL];
-#pragma unroll
-  for (int j = 0; j < CPL; ++j) {
-    const int c4 = rl + j * LPR;
-    if (c4 < E4) {
-      acc[j] = *reinterpret_cast<const d4*>(carry + own * E + c4 * 4);
-      pre[j] = Rows::load(tb, ct, r, E, c4);
-    } else {
-      acc[j] = d4{0.0, 0.0, 0.0, 0.0};
-    }
+  const int ngroups = (nchunks + kCarryGroup - 1) / kCarryGroup;
+  // Bit q of `need`: chunk base + q starts a segment left to this kernel.
+  int base;
+  uint32_t need;
+  if constexpr (LPR == kWave) {
+    // A wavefront takes a group of kCarryGroup chunks; chunk q needs a fix-up
+    // if its last segment continues in the next chunk, began in this one, and
+    // goes on past the next chunk's first 64 look-ups (one ending earlier was
+    // applied whole by the update).  Lane q examines chunk q.
+    base = (int(blockIdx.x) * kWavesPerBlock + wave_id()) * kCarryGroup;
+    if (base >= nchunks) return;
+    const int c = base + lane;
+    const uint32_t lo = uint32_t(c) * uint32_t(C);
+    const uint32_t hi = lo + uint32_t(C);
+    const bool ok = lane < kCarryGroup && c < nchunks && hi < uint32_t(NS);
+    const uint64_t wl = ok ? sorted[hi - 1] : 0ull;
+    const uint64_t wn = ok ? sorted[hi] : ~0ull;
+    const uint64_t wb = ok && lo > 0 ? sorted[lo - 1] : ~0ull;
+    const uint64_t wx =
+        ok && hi + uint32_t(kWave - 1) < uint32_t(NS) ? sorted[hi + uint32_t(kWave - 1)] : ~0ull;
+    const uint32_t kl = key_of(wl);
+    need = uint32_t(__builtin_amdgcn_ballot_w64(key_of(wn) == kl && key_of(wb) != kl &&
+                                                key_of(wx) == kl));
+  } else {
+    // A row group takes one chunk; it needs a fix-up if its last segment
+    // continues in the next chunk and began in this one.
+    base = (int(blockIdx.x) * kWavesPerBlock + wave_id()) * R + rg;
+    if (base >= nchunks) return;
+    const uint32_t lo = uint32_t(base) * uint32_t(C);
+    const uint32_t hi = min(lo + uint32_t(C), uint32_t(NS));
+    if (hi >= uint32_t(NS)) return;
+    // the words around both ends of the chunk, requested together
+    const uint64_t wl = sorted[hi - 1], wn = sorted[hi];
+    const uint64_t wb = lo > 0 ? sorted[lo - 1] : ~0ull;
+    const uint32_t kl = key_of(wl);
+    need = key_of(wn) == kl && key_of(wb) != kl ? 1u : 0u;
   }
-  // Chunks chunk+1, chunk+2, ... belong to the segment while the chunk before
-  // continues it.  At a group boundary the filled groups that follow are taken
-  // whole (the segment then continues past each): the flags of the next
-  // groups (one per lane of the row group when it has at least 16 lanes,
-  // else UF), then the sums of the leading filled ones, UF at a time, are
-  // requested and added in order.  Otherwise up to UF chunks, not crossing
-  // the next group boundary (their first-segment partials and the key just
-  // past them), are loaded per step.
   constexpr bool kLaneFlags = LPR >= 16;
   constexpr int NF = kLaneFlags ? LPR : UF;  // flags read per step
-  const int ngroups = (nchunks + kCarryGroup - 1) / kCarryGroup;
-  int unfilled = -1;  // a group known not to be filled
-  bool inside = true;
-  int c2 = chunk + 1;
-  while (inside) {
-    const int gi = c2 / kCarryGroup, off = c2 % kCarryGroup;
-    if (off == 0 && c2 < nchunks && gi != unfilled) {
-      int nf = 0;  // filled groups in a row from gi (at most NF)
-      if constexpr (kLaneFlags) {
-        const int f = gi + rl < ngroups ? gflag[gi + rl] : 0;
-        const uint64_t m = __builtin_amdgcn_ballot_w64(f != 0);
-        uint64_t mine;
-        if constexpr (LPR == kWave)
-          mine = m;
-        else
-          mine = (m >> (rg * LPR)) & ((1ull << LPR) - 1ull);
-        nf = ~mine == 0ull ? kWave : int(__builtin_ctzll(~mine));
-      } else {
+  while (need != 0) {
+    const int chunk = base + __builtin_ctz(need);
+    need &= need - 1u;
+    const uint32_t lo = uint32_t(chunk) * uint32_t(C);
+    const uint32_t hi = lo + uint32_t(C);
+    const uint32_t kl = key_of(sorted[hi - 1]);
+    const uint32_t kf = key_of(sorted[lo]);
+    const int ct = table_of_bag(bag_of(sorted[hi - 1]), B, inv_b);
+    const uint32_t r = kl - tb.rowbase[ct];
+    const int64_t own = kf != kl ? 2 * int64_t(chunk) + 1 : 2 * int64_t(chunk);
+
+    d4 acc[CPL];
+    typename Rows::Pre pre[CPL];
 #pragma unroll
-        for (int u = 0; u < UF; ++u) {
-          const int f = gi + u < ngroups ? gflag[gi + u] : 0;
-          nf += (nf == u && f != 0) ? 1 : 0;
-        }
+    for (int j = 0; j < CPL; ++j) {
+      const int c4 = rl + j * LPR;
+      if (c4 < E4) {
+        acc[j] = *reinterpret_cast<const d4*>(carry + own * E + c4 * 4);
+        pre[j] = Rows::load(tb, ct, r, E, c4);
+      } else {
+        acc[j] = d4{0.0, 0.0, 0.0, 0.0};
       }
-      if (nf < NF) unfilled = gi + nf;
-      if (nf > 0) {
-        for (int u0 = 0; u0 < nf; u0 += UF) {
-          d4 gs[UF][CPL];
+    }
+    // Chunks chunk+1, chunk+2, ... belong to the segment while the chunk
+    // before continues it.  At a group boundary the filled groups that follow
+    // are taken whole (the segment then continues past each): the flags of
+    // the next groups (one per lane of the row group when it has at least 16
+    // lanes, else UF), then the sums of the leading filled ones, UF at a time,
+    // are requested and added in order.  Otherwise up to UF chunks, not
+    // crossing the next group boundary (their first-segment partials and the
+    // key just past them), are loaded per step.
+    int unfilled = -1;  // a group known not to be filled
+    bool inside = true;
+    int c2 = chunk + 1;
+    while (inside) {
+      const int gi = c2 / kCarryGroup, off = c2 % kCarryGroup;
+      if (off == 0 && c2 < nchunks && gi != unfilled) {
+        int nf = 0;  // filled groups in a row from gi (at most NF)
+        if constexpr (kLaneFlags) {
+          const int f = gi + rl < ngroups ? gflag[gi + rl] : 0;
+          const uint64_t m = __builtin_amdgcn_ballot_w64(f != 0);
+          uint64_t mine;
+          if constexpr (LPR == kWave)
+            mine = m;
+          else
+            mine = (m >> (rg * LPR)) & ((1ull << LPR) - 1ull);
+          nf = ~mine == 0ull ? kWave : int(__builtin_ctzll(~mine));
+        } else {
 #pragma unroll
           for (int u = 0; u < UF; ++u) {
+            const int f = gi + u < ngroups ? gflag[gi + u] : 0;
+            nf += (nf == u && f != 0) ? 1 : 0;
+          }
+        }
+        if (nf < NF) unfilled = gi + nf;
+        if (nf > 0) {
+          for (int u0 = 0; u0 < nf; u0 += UF) {
+            d4 gs[UF][CPL];
 #pragma unroll
-            for (int j = 0; j < CPL; ++j) {
-              const int c4 = rl + j * LPR;
-              gs[u][j] = (u0 + u < nf && c4 < E4)
-                             ? *reinterpret_cast<const d4*>(gsum + int64_t(gi + u0 + u) * E + c4 * 4)
-                             : d4{0.0, 0.0, 0.0, 0.0};
+            for (int u = 0; u < UF; ++u) {
+#pragma unroll
+              for (int j = 0; j < CPL; ++j) {
+                const int c4 = rl + j * LPR;
+                gs[u][j] = (u0 + u < nf && c4 < E4)
+                               ? *reinterpret_cast<const d4*>(gsum + int64_t(gi + u0 + u) * E + c4 * 4)
+                               : d4{0.0, 0.0, 0.0, 0.0};
+              }
+            }
+#pragma unroll
+            for (int u = 0; u < UF; ++u) {
+              if (u0 + u >= nf) break;
+#pragma unroll
+              for (int j = 0; j < CPL; ++j) acc[j] += gs[u][j];
             }
           }
-#pragma unroll
-          for (int u = 0; u < UF; ++u) {
-            if (u0 + u >= nf) break;
-#pragma unroll
-            for (int j = 0; j < CPL; ++j) acc[j] += gs[u][j];
-          }
+          c2 += nf * kCarryGroup;
+          continue;
         }
-        c2 += nf * kCarryGroup;
-        continue;
       }
-    }
-    const int n = kCarryGroup - off < UF ? kCarryGroup - off : UF;
-    d4 part[UF][CPL];
-    uint32_t kn[UF];
+      const int n = kCarryGroup - off < UF ? kCarryGroup - off : UF;
+      d4 part[UF][CPL];
+      uint32_t kn[UF];
 #pragma unroll
-    for (int u = 0; u < UF; ++u) {
-      const int cu = c2 + u;
-      const bool ok = u < n && cu < nchunks;
-      const int64_t nxt = int64_t(cu + 1) * C;
-      kn[u] = (ok && nxt < NS) ? key_of(sorted[nxt]) : kNoKey;
+      for (int u = 0; u < UF; ++u) {
+        const int cu = c2 + u;
+        const bool ok = u < n && cu < nchunks;
+        const int64_t nxt = int64_t(cu + 1) * C;
+        kn[u] = (ok && nxt < NS) ? key_of(sorted[nxt]) : kNoKey;
 #pragma unroll
-      for (int j = 0; j < CPL; ++j) {
-        const int c4 = rl + j * LPR;
-        part[u][j] = (ok && c4 < E4) ? *reinterpret_cast<const d4*>(carry + 2 * int64_t(cu) * E + c4 * 4)
-                                     : d4{0.0, 0.0, 0.0, 0.0};
+        for (int j = 0; j < CPL; ++j) {
+          const int c4 = rl + j * LPR;
+          part[u][j] = (ok && c4 < E4) ? *reinterpret_cast<const d4*>(carry + 2 * int64_t(cu) * E + c4 * 4)
+                                       : d4{0.0, 0.0, 0.0, 0.0};
+        }
       }
+#pragma unroll
+      for (int u = 0; u < UF; ++u) {
+        if (!inside || u >= n) break;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) acc[j] += part[u][j];
+        inside = kn[u] == kl;
+      }
+      c2 += n;
     }
 #pragma unroll
-    for (int u = 0; u < UF; ++u) {
-      if (!inside || u >= n) break;
-#pragma unroll
-      for (int j = 0; j < CPL; ++j) acc[j] += part[u][j];
-      inside = kn[u] == kl;
+    for (int j = 0; j < CPL; ++j) {
+      const int c4 = rl + j * LPR;
+      if (c4 < E4) Rows::store(tb, ct, r, E, c4, pre[j], acc[j], double(lr));
     }
-    c2 += n;
-  }
-#pragma unroll
-  for (int j = 0; j < CPL; ++j) {
-    const int c4 = rl + j * LPR;
-    if (c4 < E4) Rows::store(tb, ct, r, E, c4, pre[j], acc[j], double(lr));
   }
 }
 
@@ -598,16 +705,21 @@ bool launch_apply(const TableDesc& d, int32_t B, const void* dY, float lr, const
   const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
   const float inv_b = 1.0f / float(B);
   const RowGeom g = row_geom(d.dim);
+  // a segment's end is looked for within 64 look-ups of a chunk boundary,
+  // which must stay inside the neighbouring chunk
+  if (g.lpr == kWave && L.chunk < 2 * int64_t(kWave)) return false;
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const int blocks = int((L.nchunks + per_block - 1) / per_block);
   const int32_t NS = int32_t(L.ns), C = int32_t(L.chunk), nch = int32_t(L.nchunks);
   const int32_t in_order = apply_in_dispatch_order(blocks, d.num_tables, B, d.dim, GBF16 ? 2 : 4);
+  const int fix_blocks =
+      g.lpr == kWave ? int((L.ngroups + kWavesPerBlock - 1) / kWavesPerBlock) : blocks;
   return launch_seg<Rows, MODE, GBF16>(g, blocks, st, d, sorted, NS, C, nch, dY, B, inv_b, lr,
                                        carry, flags, token, pd, in_order) &&
          launch_group(g, st, sorted, NS, C, nch, d.dim, int32_t(L.ngroups), carry, gsum, gflag,
                       flags, token) &&
-         launch_fix<Rows, MODE>(g, blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry, gsum,
-                                gflag, flags, token, pd);
+         launch_fix<Rows, MODE>(g, fix_blocks, st, d, sorted, NS, C, nch, B, inv_b, lr, carry,
+                                gsum, gflag, flags, token, pd);
 }
 
 }  // namespace

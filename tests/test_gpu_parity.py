@@ -181,6 +181,64 @@ def test_segment_past_one_flag_read(dim):
     check_step(W, batch, look, O, G, 0.1, what=f"segment past one flag read E={dim}")
 
 
+# chunk length of the sorted look-ups at these sizes (64 lanes per row: 128;
+# 16 lanes: 32; 4 lanes: 8)
+_CHUNK = {16: 8, 64: 32, 256: 128, 512: 128, 1024: 128}
+
+
+@pytest.mark.parametrize("dim,split,mode", [(16, False, "sum"), (64, False, "sum"),
+                                            (256, False, "sum"), (64, True, "sum"),
+                                            (256, True, "sum"), (64, False, "weighted"),
+                                            (256, False, "mean"), (256, False, "weighted"),
+                                            (512, False, "sum"), (1024, True, "sum")])
+def test_segments_around_the_chunk_length(dim, split, mode):
+    """Segments of 1-3 look-ups, of 63-65 (a 64-lane row's window past a chunk
+    end) and of one, two, three and sixteen chunk lengths and one look-up
+    either side, in random order.  With 64 lanes per row, a segment that ends
+    within the next chunk's first 64 look-ups is summed whole by the chunk
+    where it begins (the next chunk starts after it); all others crossing a
+    boundary go through the partial sums.  Every kind starts at every offset
+    of a chunk."""
+    import paper_2005_04680_amd as pk
+    c = _CHUNK[dim]
+    rng = np.random.default_rng(7 * dim + split + 3 * (mode != "sum"))
+    kinds = np.array([1, 2, 3, 63, 64, 65, c - 1, c, c + 1, 2 * c - 1, 2 * c, 2 * c + 1,
+                      3 * c + 5, 16 * c, 16 * c + 1, 17 * c + 3])
+    nseg = 600 if dim >= 256 else 1500
+    mult = rng.choice(kinds, nseg, p=np.r_[[0.15] * 3, [0.1] * 3, [0.2 / 7] * 7, [0.05 / 3] * 3])
+    M = nseg + 50
+    look = np.repeat(np.arange(nseg), mult).astype(np.int32)
+    rng.shuffle(look)
+    NS = look.size
+    batch = NS // 37 + 1
+    cuts = np.sort(rng.integers(0, NS + 1, batch - 1))
+    O = np.concatenate([[0], cuts, [NS]]).astype(np.int32)
+    W = _tables(rng, (M,), dim, 0.01)
+    G = rng.standard_normal((1, batch, dim)).astype(np.float32)
+    what = f"segments around C={c} E={dim} split={split} {mode}"
+    if mode == "sum":
+        check_step(W, batch, look, O, G, 0.1, split=split, what=what)
+        return
+    log(f"[parity] {what} NS={NS}")
+    a = rng.uniform(-2, 2, NS).astype(np.float32) if mode == "weighted" else None
+    pool = pk.EMBBAG_POOL_MEAN if mode == "mean" else pk.EMBBAG_POOL_SUM
+    om = oracle.POOL_MEAN if mode == "mean" else oracle.POOL_SUM
+    gt = GpuTables(W)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(1, batch, NS, dim), dtype=torch.uint8,
+                     device=DEV)
+    ad = None if a is None else to_dev(a)
+    assert pk.embbag_backward_sgd_pooled(to_dev(G), batch, to_dev(look), to_dev(O), 0.1, gt.w,
+                                         ws, ad, pool, gt.status) == 0
+    assert gt.read_status() == 0
+    Wref = [w.copy() for w in W]
+    assert oracle.backward_sgd_weighted(G, batch, look, O, 0.1, Wref, a, om) == 0
+    Wg = gt.host()[0]
+    touched = np.zeros(M, bool)
+    touched[look] = True
+    assert_close(Wg[touched], Wref[0][touched], what)
+    assert bits_equal(Wg[~touched], W[0][~touched]), f"{what}: untouched rows changed"
+
+
 def test_small_full():
     """Small-shaped workload at full size: 8 x 1e6 x 64, B=2048, P=32, Zipf(1.05)."""
     cfg = get_config("small")
