@@ -352,18 +352,18 @@ def time_graph(torch, batches, prep, fwd, apply, K, warmup):
     return {"ms_per_step": round(ms, 4), "replays": K, "graphs": len(batches)}
 
 
-def time_floor(pk, torch, tables, bt, B, NS, prep, ws, stream, K):
+def time_floor(pk, torch, touch, bt, prep, stream, K):
     """Mean ms of the update's floor on the rows of batch `bt`: every touched
-    row read and written back once (embbag_baseline_touch_rows, which leaves
-    the tables unchanged), K calls back to back on one prepared workspace
-    between two events on `stream`."""
+    row read and written back once (`touch`: embbag_baseline_touch_rows or its
+    split-storage form, which leave the tables unchanged), K calls back to
+    back on one prepared workspace between two events on `stream`."""
     pk.check(prep(bt), "prepare")
-    pk.check(pk.embbag_baseline_touch_rows(B, NS, tables, ws), "touch rows")
+    pk.check(touch(), "touch rows")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(K):
-        pk.check(pk.embbag_baseline_touch_rows(B, NS, tables, ws), "touch rows")
+        pk.check(touch(), "touch rows")
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / K
@@ -670,11 +670,15 @@ def main():
                         "pct_hbm_peak": round(100 * tb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
                         "forward_bytes": int(calls[0]), "prepare_bytes": int(calls[1]),
                         "apply_bytes": int(calls[2])}
-    if roof_call == "apply" and not split and not pooled:
+    if roof_call == "apply" and not pooled and not act_bf16:
         # The apply's floor on this GPU: the read and write-back of the same
         # touched rows with nothing summed (no gradient gathers).
         # (the rows of batch 0; its U is within 0.2% of the average)
-        floor_ms = time_floor(pk, torch, tables, batches[0], B, NS, prep, ws, main, K)
+        if split:
+            touch = lambda: pk.embbag_baseline_touch_rows_split(B, NS, hi, lo, ws)
+        else:
+            touch = lambda: pk.embbag_baseline_touch_rows(B, NS, tables, ws)
+        floor_ms = time_floor(pk, torch, touch, batches[0], prep, main, K)
         roof["floor_ms"] = round(floor_ms, 4)
         roof["floor_gbps"] = round(2 * batches[0]["U"] * E * 4 / (floor_ms * 1e-3) / 1e9, 1)
         roof["frac_of_floor"] = round(floor_ms / roof_ms, 4)

@@ -328,6 +328,15 @@ int embbag_baseline_update_owner(const float* dW, int32_t batch, const int32_t* 
 int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_tables_t* tables,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The same floor for split tables (Section VII storage): each touched row's
+ * BF16 high half and 16-bit low half are read and written back unchanged,
+ * once, as embbag_backward_apply_sgd_split_bf16 moves them.  `tables->lo`
+ * must be given; halves 8-byte aligned.  Workspace, errors and the
+ * bit-identical result as embbag_baseline_touch_rows. */
+int embbag_baseline_touch_rows_split(int32_t batch, int64_t num_indices,
+                                     const embbag_split_tables_t* tables, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
 /* Waits for `stream` and returns the device status word (*d_status), or
  * EMBBAG_ERR_HIP if the wait or copy fails. */
 int embbag_status_read(const int32_t* d_status, hipStream_t stream);

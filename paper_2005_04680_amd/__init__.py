@@ -92,6 +92,7 @@ def lib():
         L.embbag_baseline_backward_sgd_atomic.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
         L.embbag_baseline_update_owner.argtypes = [p, i32, p, p, i64, C.c_float, p, i32, p]
         L.embbag_baseline_touch_rows.argtypes = [i32, i64, p, p, sz, p]
+        L.embbag_baseline_touch_rows_split.argtypes = [i32, i64, p, p, sz, p]
         L.embbag_status_read.argtypes = [p, p]
         L.embbag_backward_sgd_noalloc.argtypes = [p, i32, p, p, i64, C.c_float, p, p, p]
         for n in ("embbag_forward", "embbag_forward_split_bf16", "embbag_backward_sgd",
@@ -104,7 +105,8 @@ def lib():
                   "embbag_split_fp32", "embbag_combine_fp32", "embbag_dedup",
                   "embbag_baseline_materialize", "embbag_baseline_update_atomic",
                   "embbag_baseline_backward_sgd_atomic", "embbag_baseline_update_owner",
-                  "embbag_baseline_touch_rows", "embbag_status_read",
+                  "embbag_baseline_touch_rows", "embbag_baseline_touch_rows_split",
+                  "embbag_status_read",
                   "embbag_backward_sgd_noalloc"):
             getattr(L, n).restype = C.c_int
         _lib = L
@@ -535,6 +537,14 @@ def embbag_baseline_touch_rows(batch, num_indices, weights, workspace, stream=No
                                             _ptr(workspace, None, "workspace"),
                                             int(workspace.numel() * workspace.element_size()),
                                             _stream(stream))
+
+
+def embbag_baseline_touch_rows_split(batch, num_indices, hi, lo, workspace, stream=None) -> int:
+    s, keep = _tables_struct(hi, split_lo=lo)
+    return lib().embbag_baseline_touch_rows_split(int(batch), int(num_indices), C.byref(s),
+                                                  _ptr(workspace, None, "workspace"),
+                                                  int(workspace.numel() * workspace.element_size()),
+                                                  _stream(stream))
 
 
 def embbag_status_read(d_status, stream=None) -> int:

@@ -546,13 +546,8 @@ int embbag_baseline_update_owner(const float* dW, int32_t batch, const int32_t* 
       launch_owner_update(d, dW, indices, offsets, num_indices, batch, owners, lr, stream));
 }
 
-int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_tables_t* tables,
-                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
-  TableDesc d;
-  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
-                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
-  if (rc) return rc;
+static int touch_common(const TableDesc& d, bool split, int32_t batch, int64_t num_indices,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (batch < 0 || num_indices < 0 || num_indices > kMaxIndices ||
       int64_t(d.num_tables) * batch + 1 > kInt32Max)
     return EMBBAG_ERR_INVALID_ARG;
@@ -561,10 +556,32 @@ int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_
   const BwdLayout L = backward_layout(d.num_tables, batch, num_indices, d.dim, total, false);
   if (workspace == nullptr || !aligned(workspace, kWsAlign) || workspace_bytes < L.total)
     return EMBBAG_ERR_WORKSPACE;
-  return hip_status(launch_touch_rows(d, batch, L, static_cast<char*>(workspace),
+  return hip_status(launch_touch_rows(d, split, batch, L, static_cast<char*>(workspace),
                                       phase_token(d.num_tables, batch, num_indices, d.dim,
                                                   total, kPoolPlain),
                                       stream));
+}
+
+int embbag_baseline_touch_rows(int32_t batch, int64_t num_indices, const embbag_tables_t* tables,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (tables == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->weights), nullptr, 16, &d);
+  if (rc) return rc;
+  return touch_common(d, false, batch, num_indices, workspace, workspace_bytes, stream);
+}
+
+int embbag_baseline_touch_rows_split(int32_t batch, int64_t num_indices,
+                                     const embbag_split_tables_t* tables, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  if (tables == nullptr || tables->lo == nullptr) return EMBBAG_ERR_INVALID_ARG;
+  TableDesc d;
+  int rc = make_desc(tables->num_tables, tables->dim, tables->rows,
+                     reinterpret_cast<void* const*>(tables->hi),
+                     reinterpret_cast<void* const*>(tables->lo), 8, &d);
+  if (rc) return rc;
+  return touch_common(d, true, batch, num_indices, workspace, workspace_bytes, stream);
 }
 
 int embbag_status_read(const int32_t* d_status, hipStream_t stream) {

@@ -13,6 +13,8 @@
 // applies each row's look-ups in increasing s, like a sequential loop.
 // A last kernel is no design of the paper but the floor of every update: the
 // read and write-back of each touched row, once, with nothing summed.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace embbag {
@@ -164,8 +166,40 @@ __global__ __launch_bounds__(kWave) void owner_update_kernel(TableDesc d,
 // walks its chunk H look-ups at a time, and for each segment that begins
 // there reads the row and writes it back unchanged (an SGD step with a zero
 // gradient), all H reads in flight before the writes.  The chunks are walked
-// in the fused update's order for FP32 gradients.
-template <int LPR, int CPL>
+// in the fused update's order for FP32 gradients.  Split rows (Section VII)
+// are read and written as their two halves, 16 bits per element each, as the
+// split update moves them.
+template <bool SPLIT>
+struct TouchRow {
+  using V = typename std::conditional<SPLIT, u2, f4>::type;
+  V a, b;
+  template <class D>
+  static __device__ __forceinline__ TouchRow load(const D& tb, int t, uint32_t r, int E, int c4) {
+    TouchRow x;
+    if constexpr (SPLIT) {
+      const size_t off = size_t(r) * E + c4 * 4;
+      x.a = __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(tb.w[t]) + off));
+      x.b = __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(tb.lo[t]) + off));
+    } else {
+      x.a = __builtin_nontemporal_load(
+          reinterpret_cast<const f4*>(static_cast<const float*>(tb.w[t]) + size_t(r) * E + c4 * 4));
+    }
+    return x;
+  }
+  template <class D>
+  __device__ __forceinline__ void store(const D& tb, int t, uint32_t r, int E, int c4) const {
+    if constexpr (SPLIT) {
+      const size_t off = size_t(r) * E + c4 * 4;
+      __builtin_nontemporal_store(a, reinterpret_cast<u2*>(static_cast<uint16_t*>(tb.w[t]) + off));
+      __builtin_nontemporal_store(b, reinterpret_cast<u2*>(static_cast<uint16_t*>(tb.lo[t]) + off));
+    } else {
+      __builtin_nontemporal_store(
+          a, reinterpret_cast<f4*>(static_cast<float*>(tb.w[t]) + size_t(r) * E + c4 * 4));
+    }
+  }
+};
+
+template <int LPR, int CPL, bool SPLIT>
 __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
     TableDesc d, const uint64_t* __restrict__ sorted, int32_t NS, int32_t C, int32_t nchunks,
     int32_t B, float inv_b, const int32_t* __restrict__ flags, uint32_t token, int32_t in_order) {
@@ -202,15 +236,13 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
       tb[u] = head[u] ? table_of_bag(bag_of(p), B, inv_b) : 0;
       row[u] = head[u] ? key - tbl.rowbase[tb[u]] : 0u;
     }
-    f4 v[H][CPL];
+    TouchRow<SPLIT> v[H][CPL];
 #pragma unroll
     for (int u = 0; u < H; ++u) {
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int c4 = rl + j * LPR;
-        if (head[u] && c4 < E4)
-          v[u][j] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(
-              static_cast<const float*>(tbl.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
+        if (head[u] && c4 < E4) v[u][j] = TouchRow<SPLIT>::load(tbl, tb[u], row[u], E, c4);
       }
     }
 #pragma unroll
@@ -218,9 +250,7 @@ __global__ __launch_bounds__(kBlock) void touch_rows_kernel(
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int c4 = rl + j * LPR;
-        if (head[u] && c4 < E4)
-          __builtin_nontemporal_store(v[u][j], reinterpret_cast<f4*>(
-              static_cast<float*>(tbl.w[tb[u]]) + size_t(row[u]) * E + c4 * 4));
+        if (head[u] && c4 < E4) v[u][j].store(tbl, tb[u], row[u], E, c4);
       }
     }
   }
@@ -301,8 +331,8 @@ hipError_t launch_owner_update(const TableDesc& d, const float* dW, const int32_
   return hipGetLastError();
 }
 
-hipError_t launch_touch_rows(const TableDesc& d, int32_t B, const BwdLayout& L, char* ws,
-                             uint32_t token, hipStream_t st) {
+hipError_t launch_touch_rows(const TableDesc& d, bool split, int32_t B, const BwdLayout& L,
+                             char* ws, uint32_t token, hipStream_t st) {
   if (L.ns == 0) return hipSuccess;
   const uint64_t* sorted = sorted_buffer(L, ws);
   const int32_t* flags = reinterpret_cast<const int32_t*>(ws + L.off_flags);
@@ -311,10 +341,15 @@ hipError_t launch_touch_rows(const TableDesc& d, int32_t B, const BwdLayout& L, 
   const int per_block = kWavesPerBlock * (kWave / g.lpr);
   const dim3 grid(unsigned((L.nchunks + per_block - 1) / per_block));
   const int32_t in_order = apply_in_dispatch_order(grid.x, d.num_tables, B, d.dim, 4);
-#define EMB_TOUCH(LL, CC)                                                                    \
-  hipLaunchKernelGGL((touch_rows_kernel<LL, CC>), grid, dim3(kBlock), 0, st, d, sorted,      \
-                     int32_t(L.ns), int32_t(L.chunk), int32_t(L.nchunks), B, inv_b, flags, token, \
-                     in_order)
+#define EMB_TOUCH(LL, CC)                                                                     \
+  if (split)                                                                                  \
+    hipLaunchKernelGGL((touch_rows_kernel<LL, CC, true>), grid, dim3(kBlock), 0, st, d, sorted, \
+                       int32_t(L.ns), int32_t(L.chunk), int32_t(L.nchunks), B, inv_b, flags,    \
+                       token, in_order);                                                      \
+  else                                                                                        \
+    hipLaunchKernelGGL((touch_rows_kernel<LL, CC, false>), grid, dim3(kBlock), 0, st, d,        \
+                       sorted, int32_t(L.ns), int32_t(L.chunk), int32_t(L.nchunks), B, inv_b,   \
+                       flags, token, in_order)
   EMB_GEOM_SWITCH(g, EMB_TOUCH)
 #undef EMB_TOUCH
   return hipGetLastError();

@@ -223,9 +223,9 @@ hipError_t launch_owner_update(const TableDesc& d, const float* dW, const int32_
                                hipStream_t st);
 
 // Floor of the update: reads and writes back (unchanged) every row that the
-// sorted look-ups of a prepared workspace touch, once.
-hipError_t launch_touch_rows(const TableDesc& d, int32_t B, const BwdLayout& L, char* ws,
-                             uint32_t token, hipStream_t st);
+// sorted look-ups of a prepared workspace touch, once (split rows: both halves).
+hipError_t launch_touch_rows(const TableDesc& d, bool split, int32_t B, const BwdLayout& L,
+                             char* ws, uint32_t token, hipStream_t st);
 
 hipError_t launch_split(const float* w, uint16_t* hi, uint16_t* lo, int64_t n, hipStream_t st);
 hipError_t launch_combine(const uint16_t* hi, const uint16_t* lo, float* w, int64_t n,

@@ -187,6 +187,14 @@ int main() {
          kInv, "dedup: no sorted keys");
   expect(embbag_baseline_touch_rows(-1, 64, &tb, ws, wsb, st), kInv, "touch rows: batch < 0");
   expect(embbag_baseline_touch_rows(8, 64, &tb, ws, 8, st), kWs, "touch rows: workspace");
+  expect(embbag_baseline_touch_rows_split(8, 64, &sp_nolo, ws, wsb, st), kInv,
+         "split touch rows: no lo");
+  expect(embbag_baseline_touch_rows_split(-1, 64, &sp, ws, wsb, st), kInv,
+         "split touch rows: batch < 0");
+  expect(embbag_baseline_touch_rows_split(8, 64, &sp, ws, 8, st), kWs,
+         "split touch rows: workspace");
+  expect(embbag_baseline_touch_rows_split(8, 64, nullptr, ws, wsb, st), kInv,
+         "split touch rows: no tables");
   expect(embbag_baseline_update_owner(G, 8, I, O, 64, 0.1f, &tb, 0, st), kInv,
          "owner update: no owners");
   expect(embbag_baseline_materialize(G, 3, 8, 16, O, 64, nullptr, stt, st), kInv,

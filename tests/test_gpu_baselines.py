@@ -98,6 +98,53 @@ def test_touch_rows_keeps_every_bit(dim):
         assert_close(a, b, f"table {t} after touch + apply")
 
 
+@pytest.mark.parametrize("dim", [16, 64, 256, 1024])
+def test_touch_rows_split_keeps_every_bit(dim):
+    """The split floor writes back both halves it read: hi and lo keep their
+    bits, and the prepared workspace still drives a split update that matches
+    the oracle's."""
+    W, I, O, G, B, E = _case(17 + dim, dim=dim, hot=0.3)
+    rows = [w.shape[0] for w in W]
+    gt = GpuTables(W, split=True)
+    hi0 = [h.clone() for h in gt.w]
+    lo0 = [l.clone() for l in gt.lo]
+    Id, Od = to_dev(I), to_dev(O)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(len(W), B, I.size, E), dtype=torch.uint8,
+                     device=DEV)
+    assert pk.embbag_backward_prepare(rows, E, B, Id, Od, ws, gt.status) == 0
+    for _ in range(2):
+        assert pk.embbag_baseline_touch_rows_split(B, I.size, gt.w, gt.lo, ws) == 0
+    for a, b in zip(gt.w + gt.lo, hi0 + lo0):
+        assert torch.equal(a, b)
+    assert pk.embbag_backward_apply_sgd_split_bf16(to_dev(G), B, I.size, 0.1, gt.w, gt.lo, ws) == 0
+    assert gt.read_status() == 0
+    his, los = zip(*[oracle.split(w) for w in W])
+    his, los = [h.copy() for h in his], [l.copy() for l in los]
+    assert oracle.backward_sgd_split(G, B, I, O, 0.1, his, los) == 0
+    for t in range(len(W)):
+        got = oracle.combine(gt.w[t].cpu().numpy().view(np.uint16), gt.lo[t].cpu().numpy().view(np.uint16))
+        want = oracle.combine(his[t], los[t])
+        assert_close(got, want, f"split table {t} after touch + apply")
+
+
+def test_touch_rows_split_writes_nothing_without_a_prepare():
+    """A workspace with no sort result for these sizes: the split floor leaves
+    the halves alone."""
+    W, I, O, G, B, E = _case(5, dim=64)
+    gt = GpuTables(W, split=True)
+    hi0 = [h.clone() for h in gt.w]
+    lo0 = [l.clone() for l in gt.lo]
+    ws = torch.zeros(pk.embbag_backward_workspace_bytes(len(W), B, I.size, E), dtype=torch.uint8,
+                     device=DEV)
+    assert pk.embbag_baseline_touch_rows_split(B, I.size, gt.w, gt.lo, ws) == 0
+    torch.cuda.synchronize()
+    for a, b in zip(gt.w + gt.lo, hi0 + lo0):
+        assert torch.equal(a, b)
+    assert (pk.embbag_baseline_touch_rows_split(B, I.size, gt.w, gt.lo, ws[:256]) ==
+            pk.EMBBAG_ERR_WORKSPACE)
+    assert pk.embbag_baseline_touch_rows_split(-1, I.size, gt.w, gt.lo, ws) == pk.EMBBAG_ERR_INVALID_ARG
+
+
 def test_touch_rows_argument_errors():
     W, I, O, G, B, E = _case(4)
     gt = GpuTables(W)
