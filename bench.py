@@ -540,32 +540,37 @@ def main():
     Y = torch.empty((T, B, E), dtype=torch.bfloat16 if act_bf16 else torch.float32, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     ws = torch.empty(pk.embbag_backward_workspace_bytes(T, B, NS, E), dtype=torch.uint8, device=dev)
+    # The tables' C descriptor, built once: per call the binding then checks
+    # only the other buffers (a list would be checked and rebuilt each call).
+    td = pk.SplitTables(hi, lo) if split else pk.Tables(tables)
 
-    def fwd(bt):
+    # (st: the stream to launch on; None: the current one, as under graph capture)
+    def fwd(bt, st=None):
         if pooled:
-            return pk.embbag_forward_pooled(tables, B, bt["I"], bt["O"], Y, bt["A"], pool_code,
-                                            status)
+            return pk.embbag_forward_pooled(td, B, bt["I"], bt["O"], Y, bt["A"], pool_code, status,
+                                            st)
         if act_bf16:
-            return pk.embbag_forward_split_bf16_act(hi, B, bt["I"], bt["O"], Y, status)
+            return pk.embbag_forward_split_bf16_act(td, B, bt["I"], bt["O"], Y, status, st)
         if split:
-            return pk.embbag_forward_split_bf16(hi, B, bt["I"], bt["O"], Y, status)
-        return pk.embbag_forward(tables, B, bt["I"], bt["O"], Y, status)
+            return pk.embbag_forward_split_bf16(td, B, bt["I"], bt["O"], Y, status, st)
+        return pk.embbag_forward(td, B, bt["I"], bt["O"], Y, status, st)
 
-    def prep(bt):
+    def prep(bt, st=None):
         if pooled:
-            return pk.embbag_backward_prepare_pooled(cfg.rows, E, B, bt["I"], bt["O"], ws, bt["A"],
-                                                     pool_code, status)
-        return pk.embbag_backward_prepare(cfg.rows, E, B, bt["I"], bt["O"], ws, status)
+            return pk.embbag_backward_prepare_pooled(td, E, B, bt["I"], bt["O"], ws, bt["A"],
+                                                     pool_code, status, st)
+        return pk.embbag_backward_prepare(td, E, B, bt["I"], bt["O"], ws, status, st)
 
-    def apply(bt):
+    def apply(bt, st=None):
         if pooled:
-            return pk.embbag_backward_apply_sgd_pooled(bt["G"], B, bt["O"], NS, cfg.lr, tables, ws,
-                                                       bt["A"], pool_code)
+            return pk.embbag_backward_apply_sgd_pooled(bt["G"], B, bt["O"], NS, cfg.lr, td, ws,
+                                                       bt["A"], pool_code, st)
         if act_bf16:
-            return pk.embbag_backward_apply_sgd_split_bf16_act(bt["G"], B, NS, cfg.lr, hi, lo, ws)
+            return pk.embbag_backward_apply_sgd_split_bf16_act(bt["G"], B, NS, cfg.lr, td, None, ws,
+                                                               st)
         if split:
-            return pk.embbag_backward_apply_sgd_split_bf16(bt["G"], B, NS, cfg.lr, hi, lo, ws)
-        return pk.embbag_backward_apply_sgd(bt["G"], B, NS, cfg.lr, tables, ws)
+            return pk.embbag_backward_apply_sgd_split_bf16(bt["G"], B, NS, cfg.lr, td, None, ws, st)
+        return pk.embbag_backward_apply_sgd(bt["G"], B, NS, cfg.lr, td, ws, st)
 
     def bwd(bt):
         rc = prep(bt)
@@ -584,16 +589,15 @@ def main():
         # beside) the forward, and its sorted look-ups are then still in the
         # MALL when the apply reads them.
         e_f0.record(main)
-        pk.check(fwd(bt), "forward")
+        pk.check(fwd(bt, main), "forward")
         e_f1.record(main)
         side.wait_event(prev)
-        with torch.cuda.stream(side):
-            e_p0.record(side)
-            pk.check(prep(bt), "prepare")
-            e_p1.record(side)
+        e_p0.record(side)
+        pk.check(prep(bt, side), "prepare")
+        e_p1.record(side)
         main.wait_event(e_p1)
         e_a0.record(main)
-        pk.check(apply(bt), "apply")
+        pk.check(apply(bt, main), "apply")
         e_a1.record(main)
         return e_a1
 
@@ -675,9 +679,9 @@ def main():
         # touched rows with nothing summed (no gradient gathers).
         # (the rows of batch 0; its U is within 0.2% of the average)
         if split:
-            touch = lambda: pk.embbag_baseline_touch_rows_split(B, NS, hi, lo, ws)
+            touch = lambda: pk.embbag_baseline_touch_rows_split(B, NS, td, None, ws)
         else:
-            touch = lambda: pk.embbag_baseline_touch_rows(B, NS, tables, ws)
+            touch = lambda: pk.embbag_baseline_touch_rows(B, NS, td, ws)
         floor_ms = time_floor(pk, torch, touch, batches[0], prep, main, K)
         roof["floor_ms"] = round(floor_ms, 4)
         roof["floor_gbps"] = round(2 * batches[0]["U"] * E * 4 / (floor_ms * 1e-3) / 1e9, 1)

@@ -15,6 +15,7 @@ Split-SGD-BF16 storage of Section VII.
 from __future__ import annotations
 
 import ctypes as C
+import functools
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -143,6 +144,7 @@ def _ptr(t, dtypes=None, name="tensor"):
     return t.data_ptr()
 
 
+@functools.lru_cache(maxsize=None)
 def _dt(*names):
     import torch
     return tuple(getattr(torch, n) for n in names if hasattr(torch, n))
@@ -177,6 +179,8 @@ def _check_act(t, T, batch, dim, name):
 
 
 def _check_tables(tables, what="table"):
+    if isinstance(tables, (Tables, SplitTables)):
+        return tables.dim
     if len(tables) == 0:
         return 0
     dim = int(tables[0].shape[1]) if len(tables[0].shape) == 2 else -1
@@ -186,7 +190,26 @@ def _check_tables(tables, what="table"):
     return dim
 
 
-def _tables_struct(tables, split_lo=None):
+_FP32_TABLES = object()  # _tables_struct's default: an FP32 entry point
+
+
+def _tables_struct(tables, split_lo=_FP32_TABLES):
+    """The C table descriptor (and the objects it points into) of FP32
+    tables, or of split tables when `split_lo` is given (None when `tables`
+    is a SplitTables)."""
+    fp32 = split_lo is _FP32_TABLES
+    if isinstance(tables, Tables):
+        if not fp32:
+            raise TypeError("FP32 Tables given where split tables (hi, lo) are expected")
+        return tables.struct, tables
+    if isinstance(tables, SplitTables):
+        if fp32:
+            raise TypeError("SplitTables given where FP32 tables are expected")
+        return tables.struct, tables
+    if fp32:
+        split_lo = None
+    else:
+        _need(split_lo is not None, "split tables need their lo halves")
     import torch
     T = len(tables)
     _check_tables(tables, "table" if split_lo is None else "hi table")
@@ -213,6 +236,10 @@ def _tables_struct(tables, split_lo=None):
 
 
 def _split_struct_fwd(hi):
+    if isinstance(hi, SplitTables):
+        return hi.struct, hi
+    if isinstance(hi, Tables):
+        raise TypeError("FP32 Tables given where split tables are expected")
     T = len(hi)
     _check_tables(hi, "hi table")
     rows = (C.c_int64 * max(T, 1))(*[int(t.shape[0]) for t in hi])
@@ -220,6 +247,60 @@ def _split_struct_fwd(hi):
     s = _SplitTables(T, int(hi[0].shape[1]) if T else 0, C.cast(rows, C.POINTER(C.c_int64)),
                      C.cast(ptrs, C.POINTER(C.c_void_p)), None)
     return s, [rows, ptrs]
+
+
+class Tables:
+    """FP32 tables (a list of [M_t, E] GPU tensors) with their C descriptor
+    checked and built once.  Every entry point that takes a list of tables
+    also takes a Tables, and then skips rebuilding the descriptor: the
+    per-call cost of the binding drops to the argument checks of the other
+    buffers.  The tensors must keep their storage while it is in use."""
+
+    def __init__(self, weights):
+        self.tensors = list(weights)
+        self.dim = _check_tables(self.tensors)
+        self.struct, self._keep = _tables_struct(self.tensors)
+        self.rows_addr = C.cast(self.struct.rows, C.c_void_p).value
+
+    def __len__(self):
+        return len(self.tensors)
+
+    def __getitem__(self, i):
+        return self.tensors[i]
+
+    def __iter__(self):
+        return iter(self.tensors)
+
+
+class SplitTables:
+    """Split tables (BF16 high halves `hi`, 16-bit low halves `lo`) with their
+    C descriptor built once; taken wherever `hi` is (its `lo` argument is
+    then ignored)."""
+
+    def __init__(self, hi, lo):
+        self.hi, self.lo = list(hi), list(lo)
+        self.dim = _check_tables(self.hi, "hi table")
+        self.struct, self._keep = _tables_struct(self.hi, split_lo=self.lo)
+        self.rows_addr = C.cast(self.struct.rows, C.c_void_p).value
+
+    def __len__(self):
+        return len(self.hi)
+
+    def __getitem__(self, i):
+        return self.hi[i]
+
+    def __iter__(self):
+        return iter(self.hi)
+
+
+def _rows_arg(rows):
+    """Rows per table as the C ABI takes them (a pointer to int64s), with the
+    array it points into: built from a list of ints, or the descriptor's own
+    when given Tables or SplitTables."""
+    if isinstance(rows, (Tables, SplitTables)):
+        return rows.rows_addr, rows
+    r = (C.c_int64 * max(len(rows), 1))(*[int(x) for x in rows])
+    return C.cast(r, C.c_void_p), r
 
 
 _I32 = ("int32",)
@@ -280,9 +361,9 @@ def embbag_backward_prepare_pooled(rows, dim, batch, indices, offsets, workspace
     _check_bags(len(rows), batch, offsets)
     _check_numel(per_sample_weights, indices.numel(), "per_sample_weights")
     T = len(rows)
-    r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
+    r, keep = _rows_arg(rows)
     return lib().embbag_backward_prepare_pooled(
-        T, C.cast(r, C.c_void_p), int(dim), int(batch), _ptr(indices, _dt(*_I32), "indices"),
+        T, r, int(dim), int(batch), _ptr(indices, _dt(*_I32), "indices"),
         _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
         _ptr(per_sample_weights, _dt("float32"), "per_sample_weights"), int(pooling),
         _ptr(workspace, None, "workspace"), int(workspace.numel() * workspace.element_size()),
@@ -367,8 +448,8 @@ def embbag_backward_prepare(rows, dim, batch, indices, offsets, workspace, d_sta
     """Phase 1 of the backward: keys, validation and the sort, into ``workspace``."""
     _check_bags(len(rows), batch, offsets)
     T = len(rows)
-    r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
-    return lib().embbag_backward_prepare(T, C.cast(r, C.c_void_p), int(dim), int(batch),
+    r, keep = _rows_arg(rows)
+    return lib().embbag_backward_prepare(T, r, int(dim), int(batch),
                                          _ptr(indices, _dt(*_I32), "indices"),
                                          _ptr(offsets, _dt(*_I32), "offsets"),
                                          int(indices.numel()), _ptr(workspace, None, "workspace"),
@@ -466,8 +547,8 @@ def embbag_dedup(rows, batch, indices, offsets, sorted_keys, sorted_bags, unique
     _check_numel(seg_off, indices.numel() + 1, "seg_off", exact=False)
     _check_numel(d_num_unique, 1, "d_num_unique", exact=False)
     T = len(rows)
-    r = (C.c_int64 * max(T, 1))(*[int(x) for x in rows])
-    return lib().embbag_dedup(T, C.cast(r, C.c_void_p), int(batch),
+    r, keep = _rows_arg(rows)
+    return lib().embbag_dedup(T, r, int(batch),
                               _ptr(indices, _dt(*_I32), "indices"),
                               _ptr(offsets, _dt(*_I32), "offsets"), int(indices.numel()),
                               _ptr(sorted_keys, _dt(*_U32), "sorted_keys"),

@@ -124,3 +124,25 @@ def test_shape_checks_before_any_library_call():
         pk.embbag_baseline_materialize(Y, 2, 3, 8, O, 6, f32(5, 8))
     with pytest.raises(ValueError, match="d_status"):
         pk.embbag_forward(W, 3, I, O, Y, i32(0))
+
+
+def test_prebuilt_descriptors_refuse_host_tensors_and_the_other_kind():
+    """Tables / SplitTables check their tensors once, when built, and an entry
+    point refuses the other kind before any library call."""
+    with pytest.raises(TypeError, match="GPU tensor"):
+        pk.Tables([torch.zeros((10, 8))])
+    h = [torch.zeros((10, 8), dtype=torch.int16)]
+    with pytest.raises(TypeError, match="GPU tensor"):
+        pk.SplitTables(h, h)
+    fp32 = pk.Tables.__new__(pk.Tables)  # as built, without touching a GPU
+    fp32.tensors, fp32.dim, fp32.struct, fp32.rows_addr = [torch.zeros((10, 8))], 8, None, 0
+    split = pk.SplitTables.__new__(pk.SplitTables)
+    split.hi, split.lo, split.dim, split.struct, split.rows_addr = h, h, 8, None, 0
+    with pytest.raises(TypeError, match="FP32 Tables"):
+        pk._tables_struct(fp32, split_lo=None)
+    with pytest.raises(TypeError, match="FP32 Tables"):
+        pk._split_struct_fwd(fp32)
+    with pytest.raises(TypeError, match="SplitTables"):
+        pk._tables_struct(split)
+    assert len(fp32) == 1 and fp32[0] is fp32.tensors[0]
+    assert len(split) == 1 and split[0] is h[0]

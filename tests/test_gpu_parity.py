@@ -593,6 +593,44 @@ def test_prepare_apply_equals_fused(split):
         assert bits_equal(a, b)
 
 
+@pytest.mark.parametrize("split", [False, True])
+def test_prebuilt_descriptors_give_the_same_bits(split):
+    """The same step through Tables / SplitTables (descriptor built once) and
+    through plain lists: bit-identical outputs and tables."""
+    rng = np.random.default_rng(31 + split)
+    rows = (500, 40, 1200)
+    W = _tables(rng, rows, 64, 0.05)
+    batch = 50
+    I, O = random_bags(rng, rows, batch, 12, empty_frac=0.1, hot_frac=0.3)
+    G = rng.standard_normal((len(rows), batch, 64)).astype(np.float32)
+    Id, Od, Gd = to_dev(I), to_dev(O), to_dev(G)
+    a, b = GpuTables(W, split=split), GpuTables(W, split=split)
+    desc = pk.SplitTables(b.w, b.lo) if split else pk.Tables(b.w)
+    Ya = torch.empty((len(rows), batch, 64), dtype=torch.float32, device=DEV)
+    Yb = torch.empty_like(Ya)
+    wsa = torch.empty(pk.embbag_backward_workspace_bytes(len(rows), batch, I.size, 64),
+                      dtype=torch.uint8, device=DEV)
+    wsb = torch.empty_like(wsa)
+    if split:
+        assert pk.embbag_forward_split_bf16(a.w, batch, Id, Od, Ya, a.status) == 0
+        assert pk.embbag_forward_split_bf16(desc, batch, Id, Od, Yb, b.status) == 0
+        assert pk.embbag_backward_prepare(list(rows), 64, batch, Id, Od, wsa, a.status) == 0
+        assert pk.embbag_backward_prepare(desc, 64, batch, Id, Od, wsb, b.status) == 0
+        assert pk.embbag_backward_apply_sgd_split_bf16(Gd, batch, I.size, 0.1, a.w, a.lo, wsa) == 0
+        assert pk.embbag_backward_apply_sgd_split_bf16(Gd, batch, I.size, 0.1, desc, None, wsb) == 0
+    else:
+        assert pk.embbag_forward(a.w, batch, Id, Od, Ya, a.status) == 0
+        assert pk.embbag_forward(desc, batch, Id, Od, Yb, b.status) == 0
+        assert pk.embbag_backward_prepare(list(rows), 64, batch, Id, Od, wsa, a.status) == 0
+        assert pk.embbag_backward_prepare(desc, 64, batch, Id, Od, wsb, b.status) == 0
+        assert pk.embbag_backward_apply_sgd(Gd, batch, I.size, 0.1, a.w, wsa) == 0
+        assert pk.embbag_backward_apply_sgd(Gd, batch, I.size, 0.1, desc, wsb) == 0
+    assert a.read_status() == 0 and b.read_status() == 0
+    assert torch.equal(Ya, Yb)
+    for x, y in zip(a.w + (a.lo or []), b.w + (b.lo or [])):
+        assert torch.equal(x, y)
+
+
 def test_apply_needs_a_prepared_workspace():
     import paper_2005_04680_amd as pk
     rng = np.random.default_rng(22)
