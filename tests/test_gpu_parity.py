@@ -631,6 +631,47 @@ def test_prebuilt_descriptors_give_the_same_bits(split):
         assert torch.equal(x, y)
 
 
+@pytest.mark.parametrize("dim", [8, 64, 256])
+def test_split_halves_not_16_byte_aligned(dim):
+    """Split halves need only 8-byte alignment (the update reads and writes
+    them 8 bytes per lane and half): halves placed 8 bytes past a 16-byte
+    boundary give the oracle's result, and the floor kernel leaves them
+    unchanged."""
+    rng = np.random.default_rng(dim + 77)
+    rows = (600, 50)
+    W = _tables(rng, rows, dim, 0.05)
+    batch = 40
+    I, O = random_bags(rng, rows, batch, 20, empty_frac=0.1, hot_frac=0.3)
+    G = rng.standard_normal((len(rows), batch, dim)).astype(np.float32)
+    his, los = zip(*[oracle.split(w) for w in W])
+    hi_d, lo_d = [], []
+    for h, l in zip(his, los):
+        for src, out in ((h, hi_d), (l, lo_d)):
+            buf = torch.empty(src.size + 4, dtype=torch.int16, device=DEV)
+            v = buf[4:].view(src.shape)  # 8 bytes past a 256-byte-aligned start
+            assert v.data_ptr() % 16 == 8
+            v.copy_(torch.from_numpy(src.view(np.int16)).to(DEV))
+            out.append(v)
+    gt = GpuTables(None, split=True, dev_tables=hi_d, dev_lo=lo_d)
+    Id, Od = to_dev(I), to_dev(O)
+    ws = torch.empty(pk.embbag_backward_workspace_bytes(len(rows), batch, I.size, dim),
+                     dtype=torch.uint8, device=DEV)
+    assert pk.embbag_backward_prepare(list(rows), dim, batch, Id, Od, ws, gt.status) == 0
+    before = [x.clone() for x in hi_d + lo_d]
+    assert pk.embbag_baseline_touch_rows_split(batch, I.size, hi_d, lo_d, ws) == 0
+    for a, b in zip(hi_d + lo_d, before):
+        assert torch.equal(a, b)
+    assert pk.embbag_backward_apply_sgd_split_bf16(to_dev(G), batch, I.size, 0.1, hi_d, lo_d,
+                                                   ws) == 0
+    assert gt.read_status() == 0
+    hr, lr_ = [h.copy() for h in his], [l.copy() for l in los]
+    assert oracle.backward_sgd_split(G, batch, I, O, 0.1, hr, lr_) == 0
+    for t in range(len(rows)):
+        got = oracle.combine(hi_d[t].cpu().numpy().view(np.uint16),
+                             lo_d[t].cpu().numpy().view(np.uint16))
+        assert_close(got, oracle.combine(hr[t], lr_[t]), f"unaligned split table {t}")
+
+
 def test_apply_needs_a_prepared_workspace():
     import paper_2005_04680_amd as pk
     rng = np.random.default_rng(22)
