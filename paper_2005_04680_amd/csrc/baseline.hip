@@ -174,27 +174,25 @@ struct TouchRow {
   using V = typename std::conditional<SPLIT, u2, f4>::type;
   V a, b;
   template <class D>
-  static __device__ __forceinline__ TouchRow load(const D& tb, int t, uint32_t r, int E, int c4) {
+  static __device__ __forceinline__ TouchRow load(const D& tb, int t, uint32_t r, uint32_t E, int c4) {
     TouchRow x;
     if constexpr (SPLIT) {
       const size_t off = size_t(r) * E + c4 * 4;
-      x.a = __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(tb.w[t]) + off));
-      x.b = __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(tb.lo[t]) + off));
+      x.a = __builtin_nontemporal_load(table_elem<const u2, uint16_t>(tb.w[t], off));
+      x.b = __builtin_nontemporal_load(table_elem<const u2, uint16_t>(tb.lo[t], off));
     } else {
-      x.a = __builtin_nontemporal_load(
-          reinterpret_cast<const f4*>(static_cast<const float*>(tb.w[t]) + size_t(r) * E + c4 * 4));
+      x.a = __builtin_nontemporal_load(table_elem<const f4, float>(tb.w[t], size_t(r) * E + c4 * 4));
     }
     return x;
   }
   template <class D>
-  __device__ __forceinline__ void store(const D& tb, int t, uint32_t r, int E, int c4) const {
+  __device__ __forceinline__ void store(const D& tb, int t, uint32_t r, uint32_t E, int c4) const {
     if constexpr (SPLIT) {
       const size_t off = size_t(r) * E + c4 * 4;
-      __builtin_nontemporal_store(a, reinterpret_cast<u2*>(static_cast<uint16_t*>(tb.w[t]) + off));
-      __builtin_nontemporal_store(b, reinterpret_cast<u2*>(static_cast<uint16_t*>(tb.lo[t]) + off));
+      __builtin_nontemporal_store(a, table_elem<u2, uint16_t>(tb.w[t], off));
+      __builtin_nontemporal_store(b, table_elem<u2, uint16_t>(tb.lo[t], off));
     } else {
-      __builtin_nontemporal_store(
-          a, reinterpret_cast<f4*>(static_cast<float*>(tb.w[t]) + size_t(r) * E + c4 * 4));
+      __builtin_nontemporal_store(a, table_elem<f4, float>(tb.w[t], size_t(r) * E + c4 * 4));
     }
   }
 };

@@ -73,6 +73,17 @@ __device__ __forceinline__ const auto& table_view(const TableDesc& d, const Tabl
     return d;
 }
 
+// Element `off` of a table (elements of type S) as a global-memory pointer to
+// V.  Table pointers that a kernel staged in LDS come back as generic
+// pointers, and a generic (flat) access counts against the LDS wait counter
+// as well as the vector-memory one: every later LDS read would wait until the
+// row loads and stores in flight had completed.  Tables are always in global
+// memory.
+template <class V, class S>
+__device__ __forceinline__ __attribute__((address_space(1))) V* table_elem(void* p, size_t off) {
+  return (__attribute__((address_space(1))) V*)(static_cast<S*>(p) + off);
+}
+
 // Lane geometry for a row of E floats: LPR lanes per row (power of two), each
 // lane owning CPL groups of 4 consecutive columns, 64/LPR rows per wavefront.
 struct RowGeom {

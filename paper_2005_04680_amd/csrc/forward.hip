@@ -21,7 +21,7 @@ namespace embbag {
 namespace {
 
 template <bool SPLIT>
-__device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, int E, int col4) {
+__device__ __forceinline__ f4 load_row4(const void* base, uint32_t row, uint32_t E, int col4) {
   if constexpr (!SPLIT) {
     const float* p = static_cast<const float*>(base) + size_t(row) * E + col4 * 4;
     return *reinterpret_cast<const f4*>(p);

@@ -43,20 +43,18 @@ struct Fp32Rows {
     f4 w;
   };
   template <class D>
-  static __device__ __forceinline__ Pre load(const D& d, int t, uint32_t r, int E, int c4) {
-    return {__builtin_nontemporal_load(
-        reinterpret_cast<const f4*>(static_cast<const float*>(d.w[t]) + size_t(r) * E + c4 * 4))};
+  static __device__ __forceinline__ Pre load(const D& d, int t, uint32_t r, uint32_t E, int c4) {
+    return {__builtin_nontemporal_load(table_elem<const f4, float>(d.w[t], size_t(r) * E + c4 * 4))};
   }
   template <class D>
-  static __device__ __forceinline__ void store(const D& d, int t, uint32_t r, int E, int c4,
+  static __device__ __forceinline__ void store(const D& d, int t, uint32_t r, uint32_t E, int c4,
                                                const Pre& p, const d4& g, double lr) {
     f4 o;
     o.x = float(double(p.w.x) - lr * g.x);
     o.y = float(double(p.w.y) - lr * g.y);
     o.z = float(double(p.w.z) - lr * g.z);
     o.w = float(double(p.w.w) - lr * g.w);
-    __builtin_nontemporal_store(
-        o, reinterpret_cast<f4*>(static_cast<float*>(d.w[t]) + size_t(r) * E + c4 * 4));
+    __builtin_nontemporal_store(o, table_elem<f4, float>(d.w[t], size_t(r) * E + c4 * 4));
   }
 };
 
@@ -67,17 +65,17 @@ struct SplitRows {
     u2 hi, lo;
   };
   template <class D>
-  static __device__ __forceinline__ Pre load(const D& d, int t, uint32_t r, int E, int c4) {
+  static __device__ __forceinline__ Pre load(const D& d, int t, uint32_t r, uint32_t E, int c4) {
     const size_t off = size_t(r) * E + c4 * 4;
-    return {__builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.w[t]) + off)),
-            __builtin_nontemporal_load(reinterpret_cast<const u2*>(static_cast<const uint16_t*>(d.lo[t]) + off))};
+    return {__builtin_nontemporal_load(table_elem<const u2, uint16_t>(d.w[t], off)),
+            __builtin_nontemporal_load(table_elem<const u2, uint16_t>(d.lo[t], off))};
   }
   static __device__ __forceinline__ float upd(uint32_t hi16, uint32_t lo16, double g, double lr) {
     const float w = __uint_as_float((hi16 << 16) | lo16);
     return float(double(w) - lr * g);
   }
   template <class D>
-  static __device__ __forceinline__ void store(const D& d, int t, uint32_t r, int E, int c4,
+  static __device__ __forceinline__ void store(const D& d, int t, uint32_t r, uint32_t E, int c4,
                                                const Pre& p, const d4& g, double lr) {
     const uint32_t w0 = __float_as_uint(upd(p.hi.x & 0xFFFFu, p.lo.x & 0xFFFFu, g.x, lr));
     const uint32_t w1 = __float_as_uint(upd(p.hi.x >> 16, p.lo.x >> 16, g.y, lr));
@@ -89,8 +87,8 @@ struct SplitRows {
     lo.x = (w0 & 0xFFFFu) | (w1 << 16);
     lo.y = (w2 & 0xFFFFu) | (w3 << 16);
     const size_t off = size_t(r) * E + c4 * 4;
-    __builtin_nontemporal_store(hi, reinterpret_cast<u2*>(static_cast<uint16_t*>(d.w[t]) + off));
-    __builtin_nontemporal_store(lo, reinterpret_cast<u2*>(static_cast<uint16_t*>(d.lo[t]) + off));
+    __builtin_nontemporal_store(hi, table_elem<u2, uint16_t>(d.w[t], off));
+    __builtin_nontemporal_store(lo, table_elem<u2, uint16_t>(d.lo[t], off));
   }
 };
 
@@ -100,7 +98,7 @@ struct SplitRows {
 template <bool GBF16>
 struct Dy {
   using Raw = typename std::conditional<GBF16, u2, f4>::type;
-  static __device__ __forceinline__ Raw load(const void* dY, uint32_t bag, int E, int c4) {
+  static __device__ __forceinline__ Raw load(const void* dY, uint32_t bag, uint32_t E, int c4) {
     if constexpr (!GBF16)
       return *reinterpret_cast<const f4*>(static_cast<const float*>(dY) + size_t(bag) * E + c4 * 4);
     else
