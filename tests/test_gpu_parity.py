@@ -339,7 +339,8 @@ def test_split_bf16_activation_argument_errors():
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("case", ["tiny", "random", "p1_hot", "small", "mlperf_scaled",
                                   "tile1024", "tile2048", "tile4096", "one_pass", "digits7",
-                                  "four_passes", "hot_17bit", "hot_24bit", "hot_2m"])
+                                  "four_passes", "hot_17bit", "hot_24bit", "hot_2m",
+                                  "empty_tables", "many_small_tables"])
 def test_dedup_bit_exact(case):
     rng = np.random.default_rng(5)
     if case == "tiny":
@@ -371,11 +372,29 @@ def test_dedup_bit_exact(case):
     elif case in ("one_pass", "digits7", "four_passes"):
         # key widths the other cases miss (the dedup needs row counts only, no
         # tables): 9-bit keys sorted in one pass, 21-bit keys in three passes of
-        # 7 bits, and 31-bit keys (1.6G rows in all) in four passes of 8 bits
+        # 7 bits, and 31-bit keys (a table of 1.6G rows) in four passes of 8 bits
         rows, batch, pool = {"one_pass": ((300, 200), 3000, 40),
                              "digits7": ((1500000, 500000), 20000, 50),
-                             "four_passes": ((2 ** 30, 1000, 2 ** 29), 5000, 60)}[case]
+                             "four_passes": ((1600000000, 1000, 3), 5000, 60)}[case]
         I, O = random_bags(rng, rows, batch, pool, 0.05, 0.3)
+    elif case == "empty_tables":
+        # tables whose bags are all empty between tables whose look-ups end
+        # inside a radix tile, and a table of one row
+        rows, batch = (50, 7, 3000, 1, 100000, 9), 400
+        I, O = random_bags(rng, rows, batch, 12, 0.1, 0.2)
+        sizes = np.diff(O.astype(np.int64)).reshape(len(rows), batch)
+        drop = np.isin(np.arange(len(rows)), (1, 5))
+        I = I[np.repeat(np.repeat(~drop, batch), sizes.reshape(-1))]
+        sizes[drop] = 0
+        O = np.zeros(len(rows) * batch + 1, np.int64)
+        np.cumsum(sizes.reshape(-1), out=O[1:])
+        O = O.astype(np.int32)
+    elif case == "many_small_tables":
+        # 64 tables, most with fewer look-ups than a radix tile, so that most
+        # tiles hold look-ups of several tables
+        rows = tuple(int(r) for r in rng.integers(1, 300000, 64))
+        batch = 37
+        I, O = random_bags(rng, rows, batch, 70, 0.2, 0.25)
     else:
         # radix tiles of 1024, 2048 and 4096 keys: 12-bit keys (6-bit digits)
         # over 300K look-ups; 17-bit keys (9-bit digits) over 400K and 3M
@@ -681,7 +700,8 @@ def test_apply_needs_a_prepared_workspace():
     G = rng.standard_normal((2, 100, 32)).astype(np.float32)
     gt = GpuTables(W)
     Id, Od, Gd = to_dev(I), to_dev(O), to_dev(G)
-    ws = torch.zeros(pk.embbag_backward_workspace_bytes(2, 100, I.size, 32), dtype=torch.uint8,
+    # sized for one look-up more (the prepare for other sizes below)
+    ws = torch.zeros(pk.embbag_backward_workspace_bytes(2, 100, I.size + 1, 32), dtype=torch.uint8,
                      device=DEV)
     # never prepared: nothing is written
     assert pk.embbag_backward_apply_sgd(Gd, 100, I.size, 0.1, gt.w, ws) == 0
