@@ -175,6 +175,12 @@ def cpu_baseline(pk, cfg, host_batches, sample_bags, act_bf16=False, pooling="su
     import oracle
     from embbag_data import table_rows_torch
 
+    # The paper's multi-core CPU designs on the same sample and tables, on all
+    # the cores this process may use (FP32 tables with plain sums only).
+    designs = not cfg.split and pooling == "sum"
+    if designs:
+        import cpu_designs
+
     P, B, T = cfg.pooling, cfg.batch, cfg.num_tables
     nb = min(sample_bags, B)
     ram = host_ram_gb()
@@ -185,9 +191,11 @@ def cpu_baseline(pk, cfg, host_batches, sample_bags, act_bf16=False, pooling="su
         full_w, full_lo = host_tables(pk, torch, cfg)
     t_fill = time.perf_counter() - t_fill
     dt, dt_f, dt_b, n_look, n_rows, n_batches = 0.0, 0.0, 0.0, 0, 0, 0
-    # one host core for the whole timed region (the oracle is single-threaded)
+    dd_f, dd_b = 0.0, 0.0
+    # one host core for the oracle's timed region (it is single-threaded)
     old_aff = os.sched_getaffinity(0)
     core = min(old_aff)
+    nthreads = len(old_aff)
     os.sched_setaffinity(0, {core})
     for batch_I, G, A in host_batches:
         if dt > budget_s:
@@ -243,6 +251,17 @@ def cpu_baseline(pk, cfg, host_batches, sample_bags, act_bf16=False, pooling="su
         dt_b += t2 - t1
         dt += t2 - t0
         assert rc1 == 0 and rc2 == 0
+        if designs:
+            os.sched_setaffinity(0, old_aff)
+            t0 = time.perf_counter()
+            rc3 = cpu_designs.forward(tabs, nb, I_s, O_s, nthreads)[0]
+            t1 = time.perf_counter()
+            rc4 = cpu_designs.backward_sgd(G_s, nb, I_s, O_s, cfg.lr, tabs, nthreads)
+            t2 = time.perf_counter()
+            os.sched_setaffinity(0, {core})
+            assert rc3 == 0 and rc4 == 0
+            dd_f += t1 - t0
+            dd_b += t2 - t1
         n_look += I_s.size
         n_batches += 1
     os.sched_setaffinity(0, old_aff)
@@ -252,14 +271,24 @@ def cpu_baseline(pk, cfg, host_batches, sample_bags, act_bf16=False, pooling="su
              f"{t_fill:.0f} s, not timed)" if full else
              f"tables compacted to the sampled look-ups' rows (host RAM {ram} GB < 1.1x "
              f"{cfg.table_bytes / 1e9:.1f} GB of tables)")
-    return {"value": n_look / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "mode": mode,
-            "sample": (f"{mode}: first {nb} of {B} bags of each of the {T} tables of batches "
-                       f"0-{n_batches - 1} ({n_look} look-ups, {n_rows} touched rows) on "
-                       f"{where}, forward + fused backward/SGD, single-threaded, {dt:.2f} s"),
-            "host": host_cpu(), "core": core,
-            "forward_lookups_per_s": round(n_look / dt_f, 1),
-            "backward_sgd_lookups_per_s": round(n_look / dt_b, 1)}
+    sample = (f"{mode}: first {nb} of {B} bags of each of the {T} tables of batches "
+              f"0-{n_batches - 1} ({n_look} look-ups, {n_rows} touched rows) on {where}")
+    res = {"value": n_look / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+           "mode": mode,
+           "sample": f"{sample}, forward + fused backward/SGD, single-threaded, {dt:.2f} s",
+           "host": host_cpu(), "core": core,
+           "forward_lookups_per_s": round(n_look / dt_f, 1),
+           "backward_sgd_lookups_per_s": round(n_look / dt_b, 1)}
+    if designs:
+        dd = dd_f + dd_b
+        res["paper_designs"] = {
+            "value": round(n_look / dd, 1), "unit": "lookups/s", "cores": nthreads,
+            "kind": ("the paper's CPU designs, OpenMP, FP32: Algorithm 1 over the bags; "
+                     "Algorithms 2-3 fused with Algorithm 4's row ownership"),
+            "sample": f"{sample}, the same look-ups after the oracle's, {dd:.2f} s",
+            "forward_lookups_per_s": round(n_look / dd_f, 1),
+            "backward_sgd_lookups_per_s": round(n_look / dd_b, 1)}
+    return res
 
 
 def calibrate_gather(pk, torch, dev, reps=10):
