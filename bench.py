@@ -453,7 +453,8 @@ def main():
     ap.add_argument("--cpu-sample-bags", type=int, default=8192,
                     help="bags per table of each sampled batch the CPU oracle is timed on")
     ap.add_argument("--cpu-sample-batches", type=int, default=3,
-                    help="batches the CPU oracle is timed on (about 10 s at the defaults)")
+                    help="batches the CPU oracle (and the paper's CPU designs) are timed on "
+                         "(about 20 s of oracle time at Large)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--overlap-prepare", action="store_true",
                     help="run the backward's index phase on a second stream, overlapped with "
