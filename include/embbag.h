@@ -33,10 +33,11 @@
  * Streams.  Every call only enqueues work on `stream` (0 = the null stream)
  *   and returns; the caller keeps all buffers alive until that work is done.
  *   The only call that waits is embbag_status_read.
- * Ownership.  The caller owns every buffer.  The library allocates no device
- *   memory, keeps no pointer after returning and holds no global state, so
- *   calls on distinct workspaces are thread-safe.  Tables are updated in
- *   place; `pooled_out` must not alias a table.
+ * Ownership.  The caller owns every buffer.  Apart from the fixed device
+ *   array of embbag_backward_sgd_noalloc (declared below), the library
+ *   allocates no device memory, keeps no pointer after returning and holds no
+ *   global state, so calls on distinct workspaces are thread-safe.  Tables are
+ *   updated in place; `pooled_out` must not alias a table.
  * Errors.  Argument errors (null pointers, sizes out of range, a workspace
  *   that is too small or misaligned) are found on the host: the call returns
  *   the code and enqueues nothing.  Data errors (bad offsets, an index out of
