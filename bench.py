@@ -267,6 +267,9 @@ def cpu_baseline(pk, cfg, host_batches, sample_bags, act_bf16=False, pooling="su
     os.sched_setaffinity(0, old_aff)
     if full:
         del full_w, full_lo
+    if n_batches == 0:
+        return {"value": None, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+                "sample": "not timed (no sampled batches)"}
     where = (f"the whole tables in host memory ({cfg.table_bytes / 1e9:.1f} GB, filled in "
              f"{t_fill:.0f} s, not timed)" if full else
              f"tables compacted to the sampled look-ups' rows (host RAM {ram} GB < 1.1x "
