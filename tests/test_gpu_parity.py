@@ -88,7 +88,7 @@ def test_row_geometries(dim):
     check_step(W, 37, I, O, G, 0.1, what=f"dim{dim}")
 
 
-@pytest.mark.parametrize("dim", [16, 64, 256])
+@pytest.mark.parametrize("dim", DIMS)
 def test_row_geometries_split(dim):
     rng = np.random.default_rng(2000 + dim)
     rows = (500, 77)
