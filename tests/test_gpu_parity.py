@@ -768,6 +768,18 @@ def test_apply_rejects_a_prepare_for_another_dim():
 @pytest.mark.parametrize("mode", ["weighted", "mean"])
 @pytest.mark.parametrize("maxp", [3, 40, 300])
 def test_weighted_and_mean(dim, mode, maxp):
+    pooled_case(dim, mode, maxp)
+
+
+@pytest.mark.parametrize("dim", [d for d in DIMS if d not in (16, 64, 128, 256, 1024)])
+@pytest.mark.parametrize("mode", ["weighted", "mean"])
+def test_weighted_and_mean_every_width(dim, mode):
+    """The pooled kernels at the row widths the test above skips (every lane
+    and column-group geometry of the forward and the update)."""
+    pooled_case(dim, mode, 40)
+
+
+def pooled_case(dim, mode, maxp):
     import paper_2005_04680_amd as pk
     rng = np.random.default_rng(dim * 3 + maxp + (mode == "mean"))
     rows = (700, 40, 3000)
