@@ -259,7 +259,9 @@ def test_split_full():
     check_step(W, cfg.batch, I, O, G, cfg.lr, split=True, what="split")
 
 
-@pytest.mark.parametrize("dim,maxp", [(16, 30), (64, 30), (128, 1), (256, 12), (1024, 5)])
+@pytest.mark.parametrize("dim,maxp", [(16, 30), (64, 30), (128, 1), (256, 12), (1024, 5),
+                                      (4, 20), (8, 20), (12, 20), (20, 20), (32, 20), (100, 20),
+                                      (260, 12), (512, 8), (768, 8)])
 def test_split_bf16_activations(dim, maxp):
     """Section VII with BF16 activations: BF16 pooled outputs from the hi halves,
     the update driven by a BF16 gradient; two-phase equals fused."""
