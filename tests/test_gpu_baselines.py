@@ -27,7 +27,7 @@ def _case(seed, rows=(2000, 37, 900), dim=64, batch=300, maxp=10, hot=0.0):
     return W, I, O, G, batch, dim
 
 
-@pytest.mark.parametrize("dim", [16, 64, 256])
+@pytest.mark.parametrize("dim", [4, 8, 12, 16, 32, 64, 100, 128, 256, 260, 512, 1024])
 def test_materialize_is_a_copy(dim):
     W, I, O, G, B, E = _case(1, dim=dim)
     T = len(W)
@@ -56,8 +56,9 @@ def test_owner_update_equals_sequential_fp32(owners, dim):
 
 
 @pytest.mark.parametrize("fused", [False, True])
-def test_atomic_update_within_tolerance(fused):
-    W, I, O, G, B, E = _case(3)
+@pytest.mark.parametrize("dim", [8, 64, 260, 1024])
+def test_atomic_update_within_tolerance(fused, dim):
+    W, I, O, G, B, E = _case(3, dim=dim)
     T = len(W)
     gt = GpuTables(W)
     if fused:
