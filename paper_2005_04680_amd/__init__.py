@@ -7,6 +7,9 @@ code.  All computation happens in the library's HIP kernels; there is no CPU
 path, and loading fails loudly when the library has not been built.  The
 buffer sizes the C ABI takes on trust (table widths, offsets, activations,
 outputs) are checked here against the call's sizes first (ValueError).
+``Tables`` (FP32) and ``SplitTables`` (hi, lo) check a list of tables and
+build its C descriptor once; every entry point accepts them where it takes a
+list, which keeps a repeated call's host cost to the call itself.
 
 Operators (arXiv 2005.04680): Algorithm 1 (sum-pooled forward), Algorithms
 2-3 fused into one backward + sparse SGD update of the touched rows, and the
