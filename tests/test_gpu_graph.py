@@ -28,11 +28,15 @@ def _same_bits(x, y):
     return torch.equal(x, y)
 
 
-@pytest.mark.parametrize("split", [False, True])
-def test_graph_replays_match_direct_launches(split):
+@pytest.mark.parametrize("split,fork", [(False, False), (True, False), (False, True),
+                                        (True, True)])
+def test_graph_replays_match_direct_launches(split, fork):
+    """With `fork`, the captured prepare is a branch of its own (a second
+    stream, joined before the apply) beside the forward, as a training step
+    may schedule it; the replays must still equal the direct launches."""
     cfg = scaled(get_config("small"), rows=20000, batch=512)
     T, B, E, NS = cfg.num_tables, cfg.batch, cfg.dim, cfg.num_indices
-    log(f"[graph] split={split} T={T} B={B} E={E} NS={NS}")
+    log(f"[graph] split={split} fork={fork} T={T} B={B} E={E} NS={NS}")
     host = [table_values_np(cfg.seed, t, np.arange(cfg.rows[t]), E, cfg.value_scale[t])
             for t in range(T)]
 
@@ -76,9 +80,26 @@ def test_graph_replays_match_direct_launches(split):
     stb = torch.zeros(1, dtype=torch.int32, device=DEV)
     torch.cuda.synchronize()
 
+    def step_fork(w, lo, bt, Y, ws, status):
+        Id, Od, Gd = bt
+        cap = torch.cuda.current_stream()
+        side = torch.cuda.Stream(device=DEV)
+        side.wait_stream(cap)
+        rc = pk.embbag_backward_prepare(cfg.rows, E, B, Id, Od, ws, status, side)
+        if split:
+            rc = rc or pk.embbag_forward_split_bf16(w, B, Id, Od, Y, status, cap)
+        else:
+            rc = rc or pk.embbag_forward(w, B, Id, Od, Y, status, cap)
+        cap.wait_stream(side)
+        if split:
+            rc = rc or pk.embbag_backward_apply_sgd_split_bf16(Gd, B, NS, cfg.lr, w, lo, ws, cap)
+        else:
+            rc = rc or pk.embbag_backward_apply_sgd(Gd, B, NS, cfg.lr, w, ws, cap)
+        return rc
+
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        rc = step(wa, la, batches[0], Ya, wsa, sta)
+        rc = (step_fork if fork else step)(wa, la, batches[0], Ya, wsa, sta)
     assert rc == 0
     torch.cuda.synchronize()
     # capture does not run the work: the tables are still the initial ones
