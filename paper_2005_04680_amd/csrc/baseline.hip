@@ -174,7 +174,8 @@ struct TouchRow {
   using V = typename std::conditional<SPLIT, u2, f4>::type;
   V a, b;
   template <class D>
-  static __device__ __forceinline__ TouchRow load(const D& tb, int t, uint32_t r, uint32_t E, int c4) {
+  static __device__ __forceinline__ TouchRow load(const D& tb, int t, uint32_t r, uint32_t E,
+                                                   int c4) {
     TouchRow x;
     if constexpr (SPLIT) {
       const size_t off = size_t(r) * E + c4 * 4;
